@@ -1,0 +1,28 @@
+/*
+ * ebrl_ops.h -- single-kernel entry points of the policy forward, exported
+ * so each hot kernel can be checked and timed on its own.
+ *
+ * Same conventions as ebrl.h: device pointers, stream-ordered, status codes.
+ */
+#ifndef EBRL_OPS_H
+#define EBRL_OPS_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* C[M, N] = A[M, K] * B[N, K]^T, the projection y = x W^T of every linear
+ * layer (W stored [out, in]).  dtype EBRL_DTYPE_BF16: A and B bf16 (MFMA
+ * path, fp32 accumulate); EBRL_DTYPE_FP32: float32.  C is float32 row-major
+ * with leading dimension N.  Requires M, N >= 1, K >= 8 and K % 8 == 0;
+ * the kernel choice (tile, split over K) depends only on (M, N, K).
+ * stream: hipStream_t or NULL. */
+int ebrl_op_gemm(int32_t dtype, const void* A, const void* B, float* C, int32_t M, int32_t N,
+                 int32_t K, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* EBRL_OPS_H */

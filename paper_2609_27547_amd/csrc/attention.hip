@@ -1,0 +1,378 @@
+// Softmax attention softmax(Q K^T / sqrt(hd) + mask) V over the paged KV
+// cache (16-token blocks), for every query head h reading KV head
+// h / (q_heads / kv_heads).
+//
+// attn_prefill_bf16: flash attention for prefill, the ViT and the flow
+//   expert.  A workgroup (4 waves) owns 64 query rows of one head; each wave
+//   computes S^T = K Q^T for its 16 queries with v_mfma_f32_16x16x32_bf16 so
+//   that every lane holds the scores of a single query, runs the online
+//   softmax in fp32 with exp2, and feeds the probabilities straight back as
+//   the B operand of O^T = V^T P^T (V staged transposed in LDS).
+// attn_prefill_f32: plain per-(query, head) kernel for fp32 policies.
+// attn_decode: one query per sequence; keys split into 64-key chunks, each
+//   chunk a workgroup that streams its K and V rows once with 16-byte loads;
+//   a second kernel combines the chunks in chunk order.
+#include <math.h>
+
+#include "kernels.h"
+
+namespace ebrl {
+
+// --------------------------------------------------------- bf16 prefill --
+
+template <int HD>
+__global__ __launch_bounds__(256) void attn_prefill_bf16_kernel(AttnPrefillArgs a, float scale_log2)
+{
+    constexpr int KT = 64;
+    constexpr int KS = HD + 8;   // sK row stride (bf16)
+    constexpr int VS = KT + 8;   // sVt row stride (bf16)
+    __shared__ __attribute__((aligned(16))) bf16_t sK[KT * KS];
+    __shared__ __attribute__((aligned(16))) bf16_t sVt[HD * VS];
+
+    const int t = blockIdx.x, h = blockIdx.y;
+    const int seq = a.tile_seq[t], qt0 = a.tile_q0[t];
+    const int env = a.seq_env[seq];
+    const int qlen = a.q_len[seq], qpos0 = a.q_pos0[seq], kvlen = a.kv_len[seq];
+    const int qoff = a.q_off[seq];
+    const int hkv = a.kv.kv_heads;
+    const int kvh = h / (a.q_heads / hkv);
+    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+    const int r = lane & 15, g = lane >> 4;
+    const int qi = qt0 + wave * 16 + r;
+    const bool qvalid = qi < qlen;
+    const int qpos = qpos0 + qi;
+
+    bf16x8 qb[HD / 32];
+    {
+        const bf16_t* qrow = (const bf16_t*)a.Q + (size_t)(qoff + min(qi, qlen - 1)) * a.ldq + h * HD;
+#pragma unroll
+        for (int ks = 0; ks < HD / 32; ++ks) {
+            uint4 v = make_uint4(0, 0, 0, 0);
+            if (qvalid) v = *reinterpret_cast<const uint4*>(qrow + ks * 32 + g * 8);
+            qb[ks] = *reinterpret_cast<bf16x8*>(&v);
+        }
+    }
+
+    int kv_end = kvlen;
+    if (a.causal) kv_end = min(kvlen, qpos0 + min(qt0 + 64, qlen));
+
+    f32x4 acc[HD / 16];
+#pragma unroll
+    for (int i = 0; i < HD / 16; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+    float m_i = -INFINITY, l_i = 0.f;
+
+    const size_t blk_elems = (size_t)2 * hkv * KV_BLOCK * HD;
+    const bf16_t* kvbase = (const bf16_t*)a.kv.base;
+    const int* bt = a.kv.block_table + (size_t)env * a.kv.bt_stride;
+
+    for (int k0 = 0; k0 < kv_end; k0 += KT) {
+        __syncthreads();
+        constexpr int CH = KT * HD / 8;
+#pragma unroll
+        for (int c = tid; c < CH; c += 256) {
+            const int key = c / (HD / 8), dc = (c % (HD / 8)) * 8;
+            const int kidx = k0 + key;
+            uint4 kv = make_uint4(0, 0, 0, 0), vv = make_uint4(0, 0, 0, 0);
+            if (kidx < kvlen) {
+                const int blk = bt[kidx >> 4];
+                const bf16_t* p = kvbase + (size_t)blk * blk_elems +
+                                  ((size_t)kvh * KV_BLOCK + (kidx & 15)) * HD + dc;
+                kv = *reinterpret_cast<const uint4*>(p);
+                vv = *reinterpret_cast<const uint4*>(p + (size_t)hkv * KV_BLOCK * HD);
+            }
+            *reinterpret_cast<uint4*>(&sK[key * KS + dc]) = kv;
+            const bf16_t* ve = reinterpret_cast<const bf16_t*>(&vv);
+#pragma unroll
+            for (int j = 0; j < 8; ++j) sVt[(dc + j) * VS + key] = ve[j];
+        }
+        __syncthreads();
+
+        // S^T tiles: lane holds key 16kt + 4g + v for query r
+        f32x4 s[4];
+#pragma unroll
+        for (int kt = 0; kt < 4; ++kt) {
+            s[kt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int ks = 0; ks < HD / 32; ++ks) {
+                const bf16x8 ka = *reinterpret_cast<const bf16x8*>(&sK[(kt * 16 + r) * KS + ks * 32 + g * 8]);
+                s[kt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka, qb[ks], s[kt], 0, 0, 0);
+            }
+        }
+        float tmax = -INFINITY;
+#pragma unroll
+        for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                const int kidx = k0 + kt * 16 + 4 * g + v;
+                const bool ok = kidx < kvlen && (!a.causal || kidx <= qpos);
+                const float val = ok ? s[kt][v] * scale_log2 : -INFINITY;
+                s[kt][v] = val;
+                tmax = fmaxf(tmax, val);
+            }
+        tmax = fmaxf(tmax, __shfl_xor(tmax, 16, 64));
+        tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
+        const float m_new = fmaxf(m_i, tmax);
+        const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
+        const float alpha = fast_exp2(m_i - m_use);
+        float psum = 0.f;
+#pragma unroll
+        for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                const float p = fast_exp2(s[kt][v] - m_use);
+                s[kt][v] = p;
+                psum += p;
+            }
+        psum += __shfl_xor(psum, 16, 64);
+        psum += __shfl_xor(psum, 32, 64);
+        l_i = l_i * alpha + psum;
+        m_i = m_new;
+#pragma unroll
+        for (int i = 0; i < HD / 16; ++i) acc[i] *= alpha;
+
+#pragma unroll
+        for (int ks2 = 0; ks2 < 2; ++ks2) {
+            bf16x8 pb;
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                pb[v] = (__bf16)s[2 * ks2][v];
+                pb[4 + v] = (__bf16)s[2 * ks2 + 1][v];
+            }
+#pragma unroll
+            for (int dt = 0; dt < HD / 16; ++dt) {
+                const bf16_t* vr = &sVt[(dt * 16 + r) * VS + ks2 * 32 + 4 * g];
+                uint4 w;
+                const uint2 lo = *reinterpret_cast<const uint2*>(vr);
+                const uint2 hi = *reinterpret_cast<const uint2*>(vr + 16);
+                w.x = lo.x; w.y = lo.y; w.z = hi.x; w.w = hi.y;
+                const bf16x8 va = *reinterpret_cast<bf16x8*>(&w);
+                acc[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, pb, acc[dt], 0, 0, 0);
+            }
+        }
+    }
+
+    if (qvalid) {
+        const float inv = l_i > 0.f ? 1.f / l_i : 0.f;
+        bf16_t* orow = (bf16_t*)a.O + (size_t)(qoff + qi) * a.ldo + h * HD;
+#pragma unroll
+        for (int dt = 0; dt < HD / 16; ++dt)
+            st4<bf16_t>(orow + dt * 16 + 4 * g, acc[dt][0] * inv, acc[dt][1] * inv,
+                        acc[dt][2] * inv, acc[dt][3] * inv);
+    }
+}
+
+// ---------------------------------------------------------- fp32 prefill --
+// grid (tile, head, 64 rows of the tile); one wave per query row.
+__global__ __launch_bounds__(64) void attn_prefill_f32_kernel(AttnPrefillArgs a, float scale)
+{
+    extern __shared__ float sh[];
+    const int t = blockIdx.x, h = blockIdx.y;
+    const int seq = a.tile_seq[t];
+    const int qi = a.tile_q0[t] + blockIdx.z;
+    const int qlen = a.q_len[seq];
+    if (qi >= qlen) return;
+    const int env = a.seq_env[seq];
+    const int hd = a.kv.head_dim, hkv = a.kv.kv_heads;
+    const int kvh = h / (a.q_heads / hkv);
+    const int qpos = a.q_pos0[seq] + qi;
+    int kvlen = a.kv_len[seq];
+    if (a.causal) kvlen = min(kvlen, qpos + 1);
+    float* q = sh;          // [hd]
+    float* sc = sh + hd;    // [kvlen]
+    const float* qrow = (const float*)a.Q + (size_t)(a.q_off[seq] + qi) * a.ldq + h * hd;
+    const int lane = threadIdx.x;
+    for (int i = lane; i < hd; i += 64) q[i] = qrow[i];
+    __syncthreads();
+    const size_t blk_elems = (size_t)2 * hkv * KV_BLOCK * hd;
+    const float* base = (const float*)a.kv.base;
+    const int* bt = a.kv.block_table + (size_t)env * a.kv.bt_stride;
+    float mx = -INFINITY;
+    for (int j = lane; j < kvlen; j += 64) {
+        const float* kr = base + (size_t)bt[j >> 4] * blk_elems + ((size_t)kvh * KV_BLOCK + (j & 15)) * hd;
+        float dot = 0.f;
+        for (int i = 0; i < hd; ++i) dot = fmaf(q[i], kr[i], dot);
+        dot *= scale;
+        sc[j] = dot;
+        mx = fmaxf(mx, dot);
+    }
+    mx = wave_max(mx);
+    float sum = 0.f;
+    for (int j = lane; j < kvlen; j += 64) {
+        const float p = expf(sc[j] - mx);
+        sc[j] = p;
+        sum += p;
+    }
+    sum = wave_sum(sum);
+    __syncthreads();
+    float* orow = (float*)a.O + (size_t)(a.q_off[seq] + qi) * a.ldo + h * hd;
+    for (int i = lane; i < hd; i += 64) {
+        float o = 0.f;
+        for (int j = 0; j < kvlen; ++j) {
+            const float* vr = base + (size_t)bt[j >> 4] * blk_elems +
+                              ((size_t)(hkv + kvh) * KV_BLOCK + (j & 15)) * hd;
+            o = fmaf(sc[j], vr[i], o);
+        }
+        orow[i] = o / sum;
+    }
+}
+
+void attn_prefill(const AttnPrefillArgs& a, hipStream_t s) {
+    if (a.n_tiles <= 0) return;
+    const int hd = a.kv.head_dim;
+    if (a.bf16) {
+        const float scale_log2 = 1.4426950408889634f / sqrtf((float)hd);
+        dim3 grid(a.n_tiles, a.q_heads);
+        if (hd == 64) hipLaunchKernelGGL(attn_prefill_bf16_kernel<64>, grid, dim3(256), 0, s, a, scale_log2);
+        else hipLaunchKernelGGL(attn_prefill_bf16_kernel<128>, grid, dim3(256), 0, s, a, scale_log2);
+    } else {
+        const float scale = 1.0f / sqrtf((float)hd);
+        dim3 grid(a.n_tiles, a.q_heads, 64);
+        const size_t shm = (size_t)(hd + a.max_kv_len) * sizeof(float);
+        hipLaunchKernelGGL(attn_prefill_f32_kernel, grid, dim3(64), shm, s, a, scale);
+    }
+}
+
+// ---------------------------------------------------------------- decode --
+
+template <typename T> EBRL_DEV void load8(const T* p, float* o);
+template <> EBRL_DEV void load8<bf16_t>(const bf16_t* p, float* o) {
+    const uint4 u = *reinterpret_cast<const uint4*>(p);
+    const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        o[2 * i] = __uint_as_float(w[i] << 16);
+        o[2 * i + 1] = __uint_as_float(w[i] & 0xFFFF0000u);
+    }
+}
+template <> EBRL_DEV void load8<float>(const float* p, float* o) {
+    const float4 a = *reinterpret_cast<const float4*>(p);
+    const float4 b = *reinterpret_cast<const float4*>(p + 4);
+    o[0] = a.x; o[1] = a.y; o[2] = a.z; o[3] = a.w;
+    o[4] = b.x; o[5] = b.y; o[6] = b.z; o[7] = b.w;
+}
+
+// grid (n, q_heads, max_splits), 256 threads
+template <typename T, int HD>
+__global__ __launch_bounds__(256) void attn_decode_split_kernel(AttnDecodeArgs a, float scale_log2)
+{
+    constexpr int CH = ATTN_DEC_CHUNK;
+    constexpr int LPK = HD / 8;          // lanes per key row
+    constexpr int KPP = 256 / LPK;       // keys per pass
+    __shared__ float sq[HD];
+    __shared__ float ss[CH];
+    __shared__ float sacc[KPP * HD];
+    __shared__ float sml[2];
+
+    const int i = blockIdx.x, h = blockIdx.y, sp = blockIdx.z;
+    const int kvlen = a.kv_len[i];
+    const int k0 = sp * CH;
+    if (k0 >= kvlen) return;
+    const int k1 = min(k0 + CH, kvlen);
+    const int nkeys = k1 - k0;
+    const int env = a.seq_env[i];
+    const int hkv = a.kv.kv_heads;
+    const int kvh = h / (a.q_heads / hkv);
+    const int tid = threadIdx.x;
+    const T* qrow = (const T*)a.Q + (size_t)i * a.ldq + h * HD;
+    for (int d = tid; d < HD; d += 256) sq[d] = ld_elem<T>(qrow + d);
+    __syncthreads();
+
+    const size_t blk_elems = (size_t)2 * hkv * KV_BLOCK * HD;
+    const T* base = (const T*)a.kv.base;
+    const int* bt = a.kv.block_table + (size_t)env * a.kv.bt_stride;
+    const int sub = tid % LPK, kg = tid / LPK;
+    const int dc = sub * 8;
+
+    for (int kk = kg; kk < CH; kk += KPP) {
+        const int kidx = k0 + kk;
+        float dot = 0.f;
+        if (kk < nkeys) {
+            const T* kr = base + (size_t)bt[kidx >> 4] * blk_elems +
+                          ((size_t)kvh * KV_BLOCK + (kidx & 15)) * HD + dc;
+            float kv[8];
+            load8<T>(kr, kv);
+#pragma unroll
+            for (int j = 0; j < 8; ++j) dot = fmaf(sq[dc + j], kv[j], dot);
+        }
+#pragma unroll
+        for (int off = LPK / 2; off > 0; off >>= 1) dot += __shfl_xor(dot, off, 64);
+        if (sub == 0) ss[kk] = (kk < nkeys) ? dot * scale_log2 : -INFINITY;
+    }
+    __syncthreads();
+    if (tid < 64) {
+        const float v = ss[tid];
+        const float m = wave_max(v);
+        const float p = (tid < nkeys) ? fast_exp2(v - m) : 0.f;
+        const float l = wave_sum(p);
+        ss[tid] = p;
+        if (tid == 0) { sml[0] = m; sml[1] = l; }
+    }
+    __syncthreads();
+    float acc[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) acc[j] = 0.f;
+    for (int kk = kg; kk < nkeys; kk += KPP) {
+        const int kidx = k0 + kk;
+        const T* vr = base + (size_t)bt[kidx >> 4] * blk_elems +
+                      ((size_t)(hkv + kvh) * KV_BLOCK + (kidx & 15)) * HD + dc;
+        float vv[8];
+        load8<T>(vr, vv);
+        const float p = ss[kk];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) acc[j] = fmaf(p, vv[j], acc[j]);
+    }
+#pragma unroll
+    for (int j = 0; j < 8; ++j) sacc[kg * HD + dc + j] = acc[j];
+    __syncthreads();
+    float* part = a.part + (((size_t)i * a.q_heads + h) * a.max_splits + sp) * (HD + 2);
+    for (int d = tid; d < HD; d += 256) {
+        float o = 0.f;
+        for (int q = 0; q < KPP; ++q) o += sacc[q * HD + d];
+        part[d] = o;
+    }
+    if (tid == 0) { part[HD] = sml[0]; part[HD + 1] = sml[1]; }
+}
+
+// grid (n, q_heads), HD threads
+template <typename T, int HD>
+__global__ void attn_decode_combine_kernel(AttnDecodeArgs a)
+{
+    const int i = blockIdx.x, h = blockIdx.y, d = threadIdx.x;
+    const int nsp = (a.kv_len[i] + ATTN_DEC_CHUNK - 1) / ATTN_DEC_CHUNK;
+    const float* part = a.part + ((size_t)i * a.q_heads + h) * a.max_splits * (HD + 2);
+    float M = -INFINITY;
+    for (int s = 0; s < nsp; ++s) M = fmaxf(M, part[s * (HD + 2) + HD]);
+    float L = 0.f, o = 0.f;
+    for (int s = 0; s < nsp; ++s) {
+        const float w = fast_exp2(part[s * (HD + 2) + HD] - M);
+        L += w * part[s * (HD + 2) + HD + 1];
+        o += w * part[s * (HD + 2) + d];
+    }
+    st_elem<T>((T*)a.O + (size_t)i * a.ldo + h * HD + d, o / L);
+}
+
+void attn_decode(const AttnDecodeArgs& a, hipStream_t s) {
+    if (a.n <= 0) return;
+    const int hd = a.kv.head_dim;
+    const float scale_log2 = 1.4426950408889634f / sqrtf((float)hd);
+    dim3 g1(a.n, a.q_heads, a.max_splits), g2(a.n, a.q_heads);
+    if (a.bf16) {
+        if (hd == 64) {
+            hipLaunchKernelGGL((attn_decode_split_kernel<bf16_t, 64>), g1, dim3(256), 0, s, a, scale_log2);
+            hipLaunchKernelGGL((attn_decode_combine_kernel<bf16_t, 64>), g2, dim3(64), 0, s, a);
+        } else {
+            hipLaunchKernelGGL((attn_decode_split_kernel<bf16_t, 128>), g1, dim3(256), 0, s, a, scale_log2);
+            hipLaunchKernelGGL((attn_decode_combine_kernel<bf16_t, 128>), g2, dim3(128), 0, s, a);
+        }
+    } else {
+        if (hd == 64) {
+            hipLaunchKernelGGL((attn_decode_split_kernel<float, 64>), g1, dim3(256), 0, s, a, scale_log2);
+            hipLaunchKernelGGL((attn_decode_combine_kernel<float, 64>), g2, dim3(64), 0, s, a);
+        } else {
+            hipLaunchKernelGGL((attn_decode_split_kernel<float, 128>), g1, dim3(256), 0, s, a, scale_log2);
+            hipLaunchKernelGGL((attn_decode_combine_kernel<float, 128>), g2, dim3(128), 0, s, a);
+        }
+    }
+}
+
+}  // namespace ebrl

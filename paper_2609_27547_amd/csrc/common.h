@@ -1,0 +1,71 @@
+// Shared device helpers of the GPU library (gfx950, wave64).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+typedef uint16_t bf16_t;  // raw bfloat16 bits in memory
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+#define EBRL_DEV __device__ __forceinline__
+
+EBRL_DEV float bf16_to_f32(bf16_t h) { return __uint_as_float(((uint32_t)h) << 16); }
+
+// Round to nearest even (finite inputs).
+EBRL_DEV bf16_t f32_to_bf16(float f) {
+    uint32_t u = __float_as_uint(f);
+    u += 0x7FFFu + ((u >> 16) & 1u);
+    return (bf16_t)(u >> 16);
+}
+
+// Element loads/stores templated on the storage type (float or bf16_t).
+template <typename T> EBRL_DEV float ld_elem(const T* p);
+template <> EBRL_DEV float ld_elem<float>(const float* p) { return *p; }
+template <> EBRL_DEV float ld_elem<bf16_t>(const bf16_t* p) { return bf16_to_f32(*p); }
+template <typename T> EBRL_DEV void st_elem(T* p, float v);
+template <> EBRL_DEV void st_elem<float>(float* p, float v) { *p = v; }
+template <> EBRL_DEV void st_elem<bf16_t>(bf16_t* p, float v) { *p = f32_to_bf16(v); }
+
+// 4 consecutive elements.
+template <typename T> EBRL_DEV void st4(T* p, float a, float b, float c, float d);
+template <> EBRL_DEV void st4<float>(float* p, float a, float b, float c, float d) {
+    *reinterpret_cast<float4*>(p) = make_float4(a, b, c, d);
+}
+template <> EBRL_DEV void st4<bf16_t>(bf16_t* p, float a, float b, float c, float d) {
+    uint2 u;
+    u.x = (uint32_t)f32_to_bf16(a) | ((uint32_t)f32_to_bf16(b) << 16);
+    u.y = (uint32_t)f32_to_bf16(c) | ((uint32_t)f32_to_bf16(d) << 16);
+    *reinterpret_cast<uint2*>(p) = u;
+}
+
+EBRL_DEV float wave_sum(float v) {
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+    return v;
+}
+
+EBRL_DEV float wave_max(float v) {
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) v = fmaxf(v, __shfl_xor(v, off, 64));
+    return v;
+}
+
+// Block-wide sum over blockDim.x threads (multiple of 64, <= 1024); every
+// thread gets the result.  `red` must hold 16 floats of shared memory.
+EBRL_DEV float block_sum(float v, float* red) {
+    v = wave_sum(v);
+    const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const int nw = blockDim.x >> 6;
+    __syncthreads();
+    if (lane == 0) red[w] = v;
+    __syncthreads();
+    float t = 0.f;
+    for (int i = 0; i < nw; ++i) t += red[i];
+    return t;
+}
+
+EBRL_DEV float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+constexpr int KV_BLOCK = 16;  // tokens per paged-KV block

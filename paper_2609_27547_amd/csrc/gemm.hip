@@ -1,0 +1,443 @@
+// Projections y = x W^T of every linear layer (W stored [out, in]).
+//
+// bf16 path: MFMA v_mfma_f32_16x16x32_bf16 tiles, LDS double buffer, fp32
+// accumulate.  The weight tile feeds the MFMA "A" operand and the activation
+// tile the "B" operand, so a lane ends up owning four consecutive output
+// columns of one row: epilogues write 8-16 contiguous bytes per lane and a
+// SwiGLU gate/up pair lands in the same lane (weights packed in 32-row
+// groups: 16 gate rows, then the 16 matching up rows).
+// fp32 path (fp32 policies): LDS-tiled FMA kernel with the same epilogues.
+// Split over K (decode-sized M): fp32 partials per split, then a reduction
+// that sums splits in a fixed order and applies the epilogue, so results do
+// not depend on timing or on the number of compute units.
+#include "kernels.h"
+
+namespace ebrl {
+
+// ------------------------------------------------------------ epilogues --
+
+struct EpiF32 {
+    float* C; int ldc;
+    EBRL_DEV void operator()(int m, int n, float a, float b, float c, float d) const {
+        st4<float>(C + (size_t)m * ldc + n, a, b, c, d);
+    }
+};
+template <typename T> struct EpiStore {
+    T* C; int ldc;
+    EBRL_DEV void operator()(int m, int n, float a, float b, float c, float d) const {
+        st4<T>(C + (size_t)m * ldc + n, a, b, c, d);
+    }
+};
+struct EpiResid {
+    float* C; int ldc;
+    EBRL_DEV void operator()(int m, int n, float a, float b, float c, float d) const {
+        float4* p = reinterpret_cast<float4*>(C + (size_t)m * ldc + n);
+        float4 r = *p;
+        r.x += a; r.y += b; r.z += c; r.w += d;
+        *p = r;
+    }
+};
+// Output row m goes to row_base[m / group] + m % group; optionally adds a
+// per-(m % group) row of `add` (position embedding).
+template <typename TA> struct EpiRemap {
+    float* C; int ldc; const int* row_base; int group; const TA* add; int add_ld;
+    EBRL_DEV void operator()(int m, int n, float a, float b, float c, float d) const {
+        int g = m / group, r = m - g * group;
+        size_t dst = (size_t)(row_base ? row_base[g] + r : m);
+        if (add) {
+            const TA* ap = add + (size_t)r * add_ld + n;
+            a += ld_elem<TA>(ap); b += ld_elem<TA>(ap + 1);
+            c += ld_elem<TA>(ap + 2); d += ld_elem<TA>(ap + 3);
+        }
+        st4<float>(C + dst * ldc + n, a, b, c, d);
+    }
+};
+EBRL_DEV float silu_f(float g) { return g / (1.0f + __expf(-g)); }
+// Paired epilogue: gate at packed column n (n % 32 < 16), up at n + 16.
+template <typename T> struct EpiSwiGLU {
+    T* H; int ldh;
+    EBRL_DEV void pair(int m, int n, const float* g, const float* u) const {
+        int col = (n >> 5) * 16 + (n & 15);
+        st4<T>(H + (size_t)m * ldh + col, silu_f(g[0]) * u[0], silu_f(g[1]) * u[1],
+               silu_f(g[2]) * u[2], silu_f(g[3]) * u[3]);
+    }
+};
+
+// ------------------------------------------------------- bf16 MFMA GEMM --
+
+constexpr int BK = 64;
+constexpr int LDSW = BK + 8;  // padded LDS row (bf16 elements)
+
+template <int BM, int BN, int WM, int WN, bool PAIRED, bool SPLIT, class Epi>
+__global__ __launch_bounds__(256) void gemm_bf16_kernel(
+    const bf16_t* __restrict__ A, int lda, const bf16_t* __restrict__ B, int ldb, int M, int N,
+    int K, int k_per_split, float* __restrict__ ws, Epi epi)
+{
+    static_assert(WM * WN == 4, "4 waves");
+    constexpr int WTM = BM / WM, WTN = BN / WN;
+    constexpr int TM = WTM / 16, TN = WTN / 16;
+    static_assert(TM >= 1 && TN >= 1, "wave tile");
+    static_assert(!PAIRED || (TN % 2 == 0), "paired epilogue needs tile pairs");
+    constexpr int A_CHUNKS = BM * (BK / 8), B_CHUNKS = BN * (BK / 8);
+    constexpr int A_ITERS = (A_CHUNKS + 255) / 256, B_ITERS = (B_CHUNKS + 255) / 256;
+
+    __shared__ __attribute__((aligned(16))) bf16_t sA[2][BM * LDSW];
+    __shared__ __attribute__((aligned(16))) bf16_t sB[2][BN * LDSW];
+
+    const int tid = threadIdx.x;
+    const int tiles_n = (N + BN - 1) / BN;
+    const int tm_idx = blockIdx.x / tiles_n, tn_idx = blockIdx.x - tm_idx * tiles_n;
+    const int m0 = tm_idx * BM, n0 = tn_idx * BN;
+    const int k_begin = blockIdx.y * k_per_split;
+    const int k_end = min(K, k_begin + k_per_split);
+    const int nk = (k_end - k_begin + BK - 1) / BK;
+
+    uint4 ra[A_ITERS], rb[B_ITERS];
+    auto load_tiles = [&](int k0) {
+#pragma unroll
+        for (int i = 0; i < A_ITERS; ++i) {
+            int c = tid + 256 * i;
+            uint4 v = make_uint4(0, 0, 0, 0);
+            if (c < A_CHUNKS) {
+                int row = c >> 3, kc = (c & 7) * 8;
+                int gr = min(m0 + row, M - 1), gk = k0 + kc;
+                if (gk < k_end) v = *reinterpret_cast<const uint4*>(A + (size_t)gr * lda + gk);
+            }
+            ra[i] = v;
+        }
+#pragma unroll
+        for (int i = 0; i < B_ITERS; ++i) {
+            int c = tid + 256 * i;
+            uint4 v = make_uint4(0, 0, 0, 0);
+            if (c < B_CHUNKS) {
+                int row = c >> 3, kc = (c & 7) * 8;
+                int gr = min(n0 + row, N - 1), gk = k0 + kc;
+                if (gk < k_end) v = *reinterpret_cast<const uint4*>(B + (size_t)gr * ldb + gk);
+            }
+            rb[i] = v;
+        }
+    };
+    auto store_tiles = [&](int buf) {
+#pragma unroll
+        for (int i = 0; i < A_ITERS; ++i) {
+            int c = tid + 256 * i;
+            if (c < A_CHUNKS) {
+                int row = c >> 3, kc = (c & 7) * 8;
+                *reinterpret_cast<uint4*>(&sA[buf][row * LDSW + kc]) = ra[i];
+            }
+        }
+#pragma unroll
+        for (int i = 0; i < B_ITERS; ++i) {
+            int c = tid + 256 * i;
+            if (c < B_CHUNKS) {
+                int row = c >> 3, kc = (c & 7) * 8;
+                *reinterpret_cast<uint4*>(&sB[buf][row * LDSW + kc]) = rb[i];
+            }
+        }
+    };
+
+    const int wave = tid >> 6, lane = tid & 63;
+    const int wm = wave / WN, wn = wave - wm * WN;
+    const int r = lane & 15, g = lane >> 4;
+
+    f32x4 acc[TM][TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    if (nk > 0) {
+        load_tiles(k_begin);
+        store_tiles(0);
+        __syncthreads();
+        for (int kt = 0; kt < nk; ++kt) {
+            const int buf = kt & 1;
+            if (kt + 1 < nk) load_tiles(k_begin + (kt + 1) * BK);
+#pragma unroll
+            for (int ks = 0; ks < BK / 32; ++ks) {
+                bf16x8 wa[TN], xb[TM];
+#pragma unroll
+                for (int j = 0; j < TN; ++j)
+                    wa[j] = *reinterpret_cast<const bf16x8*>(
+                        &sB[buf][(wn * WTN + j * 16 + r) * LDSW + ks * 32 + g * 8]);
+#pragma unroll
+                for (int i = 0; i < TM; ++i)
+                    xb[i] = *reinterpret_cast<const bf16x8*>(
+                        &sA[buf][(wm * WTM + i * 16 + r) * LDSW + ks * 32 + g * 8]);
+#pragma unroll
+                for (int i = 0; i < TM; ++i)
+#pragma unroll
+                    for (int j = 0; j < TN; ++j)
+                        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wa[j], xb[i], acc[i][j],
+                                                                            0, 0, 0);
+            }
+            if (kt + 1 < nk) store_tiles(buf ^ 1);
+            __syncthreads();
+        }
+    }
+
+    // lane owns rows m = ... + r, columns n = ... + 4g .. 4g+3 of each tile
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+        const int m = m0 + wm * WTM + i * 16 + r;
+        if (m >= M) continue;
+        if constexpr (SPLIT) {
+#pragma unroll
+            for (int j = 0; j < TN; ++j) {
+                const int n = n0 + wn * WTN + j * 16 + 4 * g;
+                if (n < N)
+                    st4<float>(ws + ((size_t)blockIdx.y * M + m) * N + n, acc[i][j][0],
+                               acc[i][j][1], acc[i][j][2], acc[i][j][3]);
+            }
+        } else if constexpr (PAIRED) {
+#pragma unroll
+            for (int j = 0; j < TN; j += 2) {
+                const int n = n0 + wn * WTN + j * 16 + 4 * g;
+                if (n < N) {
+                    float gv[4] = {acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]};
+                    float uv[4] = {acc[i][j + 1][0], acc[i][j + 1][1], acc[i][j + 1][2],
+                                   acc[i][j + 1][3]};
+                    epi.pair(m, n, gv, uv);
+                }
+            }
+        } else {
+#pragma unroll
+            for (int j = 0; j < TN; ++j) {
+                const int n = n0 + wn * WTN + j * 16 + 4 * g;
+                if (n < N) epi(m, n, acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]);
+            }
+        }
+    }
+}
+
+// ------------------------------------------------------------ fp32 GEMM --
+// 64 x 64 tile, BK 16, 256 threads; thread (ty, tx) owns rows 2ty, 2ty+1 and
+// columns grp*32 + q*4 + {0..3} and the same +16 (tx = grp*4 + q), so that a
+// SwiGLU gate/up pair is in one thread.
+template <bool PAIRED, bool SPLIT, class Epi>
+__global__ __launch_bounds__(256) void gemm_f32_kernel(const float* __restrict__ A, int lda,
+                                                       const float* __restrict__ B, int ldb, int M,
+                                                       int N, int K, int k_per_split,
+                                                       float* __restrict__ ws, Epi epi)
+{
+    constexpr int TBM = 64, TBN = 64, TBK = 16;
+    __shared__ float sA[TBK][TBM + 4];
+    __shared__ float sB[TBK][TBN + 4];
+    const int tid = threadIdx.x;
+    const int tiles_n = (N + TBN - 1) / TBN;
+    const int tmi = blockIdx.x / tiles_n, tni = blockIdx.x - tmi * tiles_n;
+    const int m0 = tmi * TBM, n0 = tni * TBN;
+    const int k_begin = blockIdx.y * k_per_split;
+    const int k_end = min(K, k_begin + k_per_split);
+    const int ty = tid >> 3, tx = tid & 7;
+    const int grp = tx >> 2, q = tx & 3;
+    int cols[8];
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+        cols[c] = grp * 32 + q * 4 + c;
+        cols[4 + c] = grp * 32 + 16 + q * 4 + c;
+    }
+    float acc[2][8];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int c = 0; c < 8; ++c) acc[i][c] = 0.f;
+
+    for (int k0 = k_begin; k0 < k_end; k0 += TBK) {
+        // 64 x 16 elements of A and of B: 4 per thread each
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            int e = tid + 256 * i;
+            int row = e >> 4, kk = e & 15;
+            int gk = k0 + kk;
+            float va = 0.f, vb = 0.f;
+            if (gk < k_end) {
+                va = A[(size_t)min(m0 + row, M - 1) * lda + gk];
+                vb = B[(size_t)min(n0 + row, N - 1) * ldb + gk];
+            }
+            sA[kk][row] = va;
+            sB[kk][row] = vb;
+        }
+        __syncthreads();
+#pragma unroll
+        for (int kk = 0; kk < TBK; ++kk) {
+            float a0 = sA[kk][2 * ty], a1 = sA[kk][2 * ty + 1];
+#pragma unroll
+            for (int c = 0; c < 8; ++c) {
+                float b = sB[kk][cols[c]];
+                acc[0][c] = fmaf(a0, b, acc[0][c]);
+                acc[1][c] = fmaf(a1, b, acc[1][c]);
+            }
+        }
+        __syncthreads();
+    }
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+        const int m = m0 + 2 * ty + i;
+        if (m >= M) continue;
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            const int n = n0 + cols[4 * h];
+            if (n >= N) continue;
+            float* v = &acc[i][4 * h];
+            if constexpr (SPLIT) {
+                st4<float>(ws + ((size_t)blockIdx.y * M + m) * N + n, v[0], v[1], v[2], v[3]);
+            } else if constexpr (PAIRED) {
+                if (h == 0) epi.pair(m, n, &acc[i][0], &acc[i][4]);
+            } else {
+                epi(m, n, v[0], v[1], v[2], v[3]);
+            }
+        }
+    }
+}
+
+// Sum split partials in split order, then apply the epilogue.  One thread
+// per (row, 4 output columns); for paired epilogues the output columns are
+// the gate columns (packed n % 32 < 16).
+template <bool PAIRED, class Epi>
+__global__ void splitk_reduce_kernel(const float* __restrict__ ws, int splits, int M, int N,
+                                     Epi epi)
+{
+    const int groups = PAIRED ? N / 8 : N / 4;
+    const long total = (long)M * groups;
+    for (long idx = blockIdx.x * (long)blockDim.x + threadIdx.x; idx < total;
+         idx += (long)gridDim.x * blockDim.x) {
+        const int m = (int)(idx / groups);
+        const int gq = (int)(idx - (long)m * groups);
+        int n;
+        if (PAIRED) n = (gq >> 2) * 32 + (gq & 3) * 4;
+        else n = gq * 4;
+        float v[4] = {0.f, 0.f, 0.f, 0.f}, u[4] = {0.f, 0.f, 0.f, 0.f};
+        for (int s = 0; s < splits; ++s) {
+            const float4 a = *reinterpret_cast<const float4*>(ws + ((size_t)s * M + m) * N + n);
+            v[0] += a.x; v[1] += a.y; v[2] += a.z; v[3] += a.w;
+            if (PAIRED) {
+                const float4 b =
+                    *reinterpret_cast<const float4*>(ws + ((size_t)s * M + m) * N + n + 16);
+                u[0] += b.x; u[1] += b.y; u[2] += b.z; u[3] += b.w;
+            }
+        }
+        if constexpr (PAIRED) epi.pair(m, n, v, u);
+        else epi(m, n, v[0], v[1], v[2], v[3]);
+    }
+}
+
+// ------------------------------------------------------------- dispatch --
+
+// Tile and split choice depend only on (M, N, K).
+struct GemmPlan { int bm; int splits; int k_per_split; };
+
+static GemmPlan plan_gemm(bool bf16, int M, int N, int K, size_t ws_floats) {
+    GemmPlan p;
+    if (!bf16) p.bm = 64;
+    else if (M <= 16) p.bm = 16;
+    else if (M <= 32) p.bm = 32;
+    else if (M <= 64) p.bm = 64;
+    else p.bm = 128;
+    const int bn = bf16 ? (p.bm == 16 ? 256 : 128) : 64;
+    const long tiles = (long)((M + p.bm - 1) / p.bm) * ((N + bn - 1) / bn);
+    int splits = 1;
+    if (tiles < 256) {
+        const int kblocks = (K + BK - 1) / BK;
+        splits = (int)std::min<long>((512 + tiles - 1) / tiles, (long)std::max(1, kblocks / 2));
+        splits = std::max(1, std::min(splits, 16));
+    }
+    while (splits > 1 && (size_t)splits * M * N > ws_floats) --splits;
+    int kps = (K + splits - 1) / splits;
+    kps = (kps + BK - 1) / BK * BK;
+    splits = (K + kps - 1) / kps;
+    p.splits = splits;
+    p.k_per_split = kps;
+    return p;
+}
+
+template <bool PAIRED, class Epi>
+static void launch_bf16(const GemmArgs& a, const GemmPlan& p, Epi epi, hipStream_t s) {
+    const bool split = p.splits > 1;
+    auto go = [&](auto kern, int bm, int bn) {
+        dim3 grid(((a.M + bm - 1) / bm) * ((a.N + bn - 1) / bn), p.splits);
+        hipLaunchKernelGGL(kern, grid, dim3(256), 0, s, (const bf16_t*)a.A, a.lda,
+                           (const bf16_t*)a.B, a.ldb, a.M, a.N, a.K, p.k_per_split, a.ws, epi);
+    };
+    switch (p.bm) {
+    case 16:
+        if (split) go(gemm_bf16_kernel<16, 256, 1, 4, PAIRED, true, Epi>, 16, 256);
+        else go(gemm_bf16_kernel<16, 256, 1, 4, PAIRED, false, Epi>, 16, 256);
+        break;
+    case 32:
+        if (split) go(gemm_bf16_kernel<32, 128, 1, 4, PAIRED, true, Epi>, 32, 128);
+        else go(gemm_bf16_kernel<32, 128, 1, 4, PAIRED, false, Epi>, 32, 128);
+        break;
+    case 64:
+        if (split) go(gemm_bf16_kernel<64, 128, 1, 4, PAIRED, true, Epi>, 64, 128);
+        else go(gemm_bf16_kernel<64, 128, 1, 4, PAIRED, false, Epi>, 64, 128);
+        break;
+    default:
+        if (split) go(gemm_bf16_kernel<128, 128, 2, 2, PAIRED, true, Epi>, 128, 128);
+        else go(gemm_bf16_kernel<128, 128, 2, 2, PAIRED, false, Epi>, 128, 128);
+        break;
+    }
+    if (split) {
+        const int groups = PAIRED ? a.N / 8 : a.N / 4;
+        long total = (long)a.M * groups;
+        int blocks = (int)std::min<long>((total + 255) / 256, 4096);
+        hipLaunchKernelGGL((splitk_reduce_kernel<PAIRED, Epi>), dim3(blocks), dim3(256), 0, s,
+                           a.ws, p.splits, a.M, a.N, epi);
+    }
+}
+
+template <bool PAIRED, class Epi>
+static void launch_f32(const GemmArgs& a, const GemmPlan& p, Epi epi, hipStream_t s) {
+    dim3 grid(((a.M + 63) / 64) * ((a.N + 63) / 64), p.splits);
+    if (p.splits > 1) {
+        hipLaunchKernelGGL((gemm_f32_kernel<PAIRED, true, Epi>), grid, dim3(256), 0, s,
+                           (const float*)a.A, a.lda, (const float*)a.B, a.ldb, a.M, a.N, a.K,
+                           p.k_per_split, a.ws, epi);
+        const int groups = PAIRED ? a.N / 8 : a.N / 4;
+        long total = (long)a.M * groups;
+        int blocks = (int)std::min<long>((total + 255) / 256, 4096);
+        hipLaunchKernelGGL((splitk_reduce_kernel<PAIRED, Epi>), dim3(blocks), dim3(256), 0, s,
+                           a.ws, p.splits, a.M, a.N, epi);
+    } else {
+        hipLaunchKernelGGL((gemm_f32_kernel<PAIRED, false, Epi>), grid, dim3(256), 0, s,
+                           (const float*)a.A, a.lda, (const float*)a.B, a.ldb, a.M, a.N, a.K,
+                           p.k_per_split, a.ws, epi);
+    }
+}
+
+template <bool PAIRED, class Epi>
+static int dispatch(const GemmArgs& a, Epi epi, hipStream_t s) {
+    const GemmPlan p = plan_gemm(a.bf16, a.M, a.N, a.K, a.ws_floats);
+    if (a.bf16) launch_bf16<PAIRED>(a, p, epi, s);
+    else launch_f32<PAIRED>(a, p, epi, s);
+    return p.splits;
+}
+
+int gemm(const GemmArgs& a, hipStream_t s) {
+    if (a.M <= 0 || a.N <= 0) return 0;
+    switch (a.epi) {
+    case EPI_F32:
+        return dispatch<false>(a, EpiF32{(float*)a.C, a.ldc}, s);
+    case EPI_ACT:
+        if (a.bf16) return dispatch<false>(a, EpiStore<bf16_t>{(bf16_t*)a.C, a.ldc}, s);
+        return dispatch<false>(a, EpiStore<float>{(float*)a.C, a.ldc}, s);
+    case EPI_RESID:
+        return dispatch<false>(a, EpiResid{(float*)a.C, a.ldc}, s);
+    case EPI_REMAP:
+        if (a.bf16)
+            return dispatch<false>(a, EpiRemap<bf16_t>{(float*)a.C, a.ldc, a.row_base, a.group,
+                                                       (const bf16_t*)a.add, a.add_ld}, s);
+        return dispatch<false>(a, EpiRemap<float>{(float*)a.C, a.ldc, a.row_base, a.group,
+                                                  (const float*)a.add, a.add_ld}, s);
+    case EPI_SWIGLU:
+        if (a.bf16) return dispatch<true>(a, EpiSwiGLU<bf16_t>{(bf16_t*)a.C, a.ldc}, s);
+        return dispatch<true>(a, EpiSwiGLU<float>{(float*)a.C, a.ldc}, s);
+    }
+    return 0;
+}
+
+int gemm_splits(bool bf16, int M, int N, int K, size_t ws_floats) {
+    return plan_gemm(bf16, M, N, K, ws_floats).splits;
+}
+
+}  // namespace ebrl

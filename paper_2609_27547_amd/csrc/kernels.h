@@ -1,0 +1,147 @@
+// Launch wrappers of the GPU library's kernels (host-callable).
+#pragma once
+
+#include <algorithm>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "common.h"
+
+namespace ebrl {
+
+// ------------------------------------------------------------------ GEMM --
+enum EpiKind {
+    EPI_F32 = 0,     // C f32 [M, ldc] = acc
+    EPI_ACT = 1,     // C act dtype = acc (bf16 or f32)
+    EPI_RESID = 2,   // C f32 += acc (residual stream)
+    EPI_REMAP = 3,   // C f32 row row_base[m/group] + m%group = acc (+ add row m%group)
+    EPI_SWIGLU = 4   // packed gate/up -> C act [M, N/2] = silu(gate) * up
+};
+
+struct GemmArgs {
+    bool bf16 = true;
+    const void* A = nullptr; int lda = 0;   // [M, K] activations
+    const void* B = nullptr; int ldb = 0;   // [N, K] weights
+    int M = 0, N = 0, K = 0;
+    EpiKind epi = EPI_F32;
+    void* C = nullptr; int ldc = 0;
+    const int* row_base = nullptr; int group = 1;
+    const void* add = nullptr; int add_ld = 0;
+    float* ws = nullptr; size_t ws_floats = 0;  // split-K workspace
+};
+// Returns the number of K splits used (1 = single pass).
+int gemm(const GemmArgs& a, hipStream_t s);
+int gemm_splits(bool bf16, int M, int N, int K, size_t ws_floats);
+
+// ------------------------------------------------------------- attention --
+// Paged KV: layer base pointer; physical block b holds
+// [2 (K, V)][kv_heads][16 tokens][head_dim] elements.
+struct PagedKV {
+    void* base = nullptr;            // this layer's first block
+    const int* block_table = nullptr;  // [max_envs][bt_stride]
+    int bt_stride = 0;
+    int kv_heads = 0, head_dim = 0;
+};
+
+// Flash attention over query tiles of 64 rows.  Tile t covers rows
+// [tile_q0[t], +64) of sequence tile_seq[t].
+struct AttnPrefillArgs {
+    bool bf16 = true;
+    const void* Q = nullptr; int ldq = 0;  // [rows, q_heads*hd]
+    void* O = nullptr; int ldo = 0;        // [rows, q_heads*hd]
+    int q_heads = 0;
+    PagedKV kv;
+    const int* seq_env = nullptr;   // [n] block-table row of each sequence
+    const int* q_off = nullptr;     // [n] first Q/O row
+    const int* q_len = nullptr;     // [n]
+    const int* q_pos0 = nullptr;    // [n] absolute position of the first query
+    const int* kv_len = nullptr;    // [n]
+    const int* tile_seq = nullptr;  // [n_tiles]
+    const int* tile_q0 = nullptr;   // [n_tiles]
+    int n_tiles = 0;
+    bool causal = true;
+    int max_kv_len = 0;             // fp32 path: scores buffer size
+};
+void attn_prefill(const AttnPrefillArgs& a, hipStream_t s);
+
+// One query per sequence against kv_len[i] keys, split over the sequence
+// in chunks of ATTN_DEC_CHUNK keys, then combined in chunk order.
+constexpr int ATTN_DEC_CHUNK = 64;
+struct AttnDecodeArgs {
+    bool bf16 = true;
+    const void* Q = nullptr; int ldq = 0;  // [n, q_heads*hd]
+    void* O = nullptr; int ldo = 0;
+    int q_heads = 0;
+    PagedKV kv;
+    const int* seq_env = nullptr;
+    const int* kv_len = nullptr;
+    int n = 0;
+    int max_splits = 0;            // ceil(max kv_len / chunk) over the call
+    float* part = nullptr;         // [n][q_heads][max_splits][hd + 2]
+};
+void attn_decode(const AttnDecodeArgs& a, hipStream_t s);
+
+// ----------------------------------------------------------------- misc --
+// Y[row] = rmsnorm(X[src_row]) ; src_row = rows ? rows[i] : i
+void rmsnorm_rows(bool bf16_out, const float* X, int ldx, const int* rows, void* Y, int ldy,
+                  int n_rows, int d, float eps, hipStream_t s);
+
+// Split the fused QKV projection (f32, [M, (hq + 2 hkv) hd]) into rotated
+// queries (act dtype) and rotated keys + values written to the paged cache
+// at (seq_env[row_seq[m]], row_pos[m]).  use_rope = false skips rotation.
+struct RopeKVArgs {
+    bool bf16 = true;
+    const float* qkv = nullptr; int ld = 0;
+    int M = 0, q_heads = 0;
+    void* Q = nullptr; int ldq = 0;
+    PagedKV kv;
+    const int* seq_env = nullptr;
+    const int* row_seq = nullptr;
+    const int* row_pos = nullptr;
+    const float* cos_tab = nullptr;  // [max_pos][hd/2]
+    const float* sin_tab = nullptr;
+    bool use_rope = true;
+};
+void rope_kv_write(const RopeKVArgs& a, hipStream_t s);
+
+// X[dst] = E[id] as float (id = ids[src ? src[i] : i*stride + off]; dst = dst_rows ? dst_rows[i] : i);
+// ids outside [0, n_rows_e) give zero rows.
+void embed_rows(bool bf16, const void* E, int n_rows_e, int d, const int* ids, const int* src, int stride,
+                int off, const int* dst_rows, float* X, int ldx, int n, hipStream_t s);
+
+// images f32 [n, cams, H, W, 3] -> patches [n*cams*(H/P)*(W/P), kpad] (zero-padded columns)
+void im2col(bool bf16, const float* img, int n, int cams, int H, int W, int P, void* out,
+            int kpad, hipStream_t s);
+
+// Action head: logits = W_act . rmsnorm(x_row), argmax (ties -> lowest), top-2 margin,
+// bin -> action.  Writes column `col` of [n, ntok] outputs.
+struct LogitsArgs {
+    bool bf16 = true;
+    const float* X = nullptr; int ldx = 0;
+    const int* rows = nullptr;      // gather rows of X (nullable: identity)
+    const void* W = nullptr;        // [n_bins, d]
+    int d = 0, n_bins = 256, n = 0;
+    float eps = 1e-6f;
+    int* tokens = nullptr; float* actions = nullptr; float* margins = nullptr;
+    int ntok = 7, col = 0;
+};
+void action_logits(const LogitsArgs& a, hipStream_t s);
+
+// Last prefix row of each sequence: h_pre[env] = X[row]; h_norm[env] = rmsnorm(X[row]).
+void gather_last(const float* X, int ldx, const int* seq_env, const int* last_row, int n, int d,
+                 float eps, float* h_pre, float* h_norm, hipStream_t s);
+
+// out[r][n] = sum_k in[r][k] * W[n][k]  (W act dtype), optional silu on the input.
+void small_linear(bool bf16, const float* in, int R, int K, const void* W, int N, float* out,
+                  bool silu_input, hipStream_t s);
+
+// Flow-matching expert input and Euler update.
+void flow_in(bool bf16, const float* x, int rows, int adim, const void* W_ain, const float* tvec,
+             int d, float* H, int ldh, hipStream_t s);
+void flow_out(bool bf16, const float* H, int ldh, int rows, int d, const void* W_aout, int adim,
+              float eps, float n_steps, float* x, float* v_out, hipStream_t s);
+
+// Element copy (device) with f32 -> f32.
+void copy_f32(const float* src, float* dst, size_t n, hipStream_t s);
+
+}  // namespace ebrl

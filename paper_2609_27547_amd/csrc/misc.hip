@@ -1,0 +1,383 @@
+// Row-wise kernels of the policy forward: RMSNorm, rotary embedding with the
+// paged-KV write, embedding gathers, patch extraction, the 256-bin action
+// head with its argmax, and the flow-matching expert's input and Euler
+// update.  All reductions run in a fixed order (deterministic results).
+#include <math.h>
+
+#include "kernels.h"
+
+namespace ebrl {
+
+template <typename T> EBRL_DEV void load8v(const T* p, float* o);
+template <> EBRL_DEV void load8v<bf16_t>(const bf16_t* p, float* o) {
+    const uint4 u = *reinterpret_cast<const uint4*>(p);
+    const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        o[2 * i] = __uint_as_float(w[i] << 16);
+        o[2 * i + 1] = __uint_as_float(w[i] & 0xFFFF0000u);
+    }
+}
+template <> EBRL_DEV void load8v<float>(const float* p, float* o) {
+    const float4 a = *reinterpret_cast<const float4*>(p);
+    const float4 b = *reinterpret_cast<const float4*>(p + 4);
+    o[0] = a.x; o[1] = a.y; o[2] = a.z; o[3] = a.w;
+    o[4] = b.x; o[5] = b.y; o[6] = b.z; o[7] = b.w;
+}
+
+// sum of squares of a row (fixed order), then 1/sqrt(mean + eps)
+EBRL_DEV float row_rstd(const float* x, int d, float eps, float* red) {
+    float ss = 0.f;
+    for (int j = threadIdx.x * 4; j < d; j += blockDim.x * 4) {
+        const float4 v = *reinterpret_cast<const float4*>(x + j);
+        ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+    }
+    ss = block_sum(ss, red);
+    return 1.0f / sqrtf(ss / (float)d + eps);
+}
+
+// ------------------------------------------------------------- RMSNorm --
+template <typename TO>
+__global__ __launch_bounds__(256) void rmsnorm_kernel(const float* X, int ldx, const int* rows, TO* Y,
+                                                      int ldy, int d, float eps)
+{
+    __shared__ float red[16];
+    const int i = blockIdx.x;
+    const int src = rows ? rows[i] : i;
+    const float* x = X + (size_t)src * ldx;
+    const float rs = row_rstd(x, d, eps, red);
+    TO* y = Y + (size_t)i * ldy;
+    for (int j = threadIdx.x * 4; j < d; j += blockDim.x * 4) {
+        const float4 v = *reinterpret_cast<const float4*>(x + j);
+        st4<TO>(y + j, v.x * rs, v.y * rs, v.z * rs, v.w * rs);
+    }
+}
+
+void rmsnorm_rows(bool bf16_out, const float* X, int ldx, const int* rows, void* Y, int ldy,
+                  int n_rows, int d, float eps, hipStream_t s) {
+    if (n_rows <= 0) return;
+    if (bf16_out)
+        hipLaunchKernelGGL(rmsnorm_kernel<bf16_t>, dim3(n_rows), dim3(256), 0, s, X, ldx, rows,
+                           (bf16_t*)Y, ldy, d, eps);
+    else
+        hipLaunchKernelGGL(rmsnorm_kernel<float>, dim3(n_rows), dim3(256), 0, s, X, ldx, rows,
+                           (float*)Y, ldy, d, eps);
+}
+
+// ------------------------------------------------------ rotary + KV write --
+template <typename T>
+__global__ __launch_bounds__(256) void rope_kv_kernel(RopeKVArgs a)
+{
+    const int m = blockIdx.x;
+    const int hd = a.kv.head_dim, half = hd / 2;
+    const int hq = a.q_heads, hkv = a.kv.kv_heads;
+    const int seq = a.row_seq[m], pos = a.row_pos[m];
+    const int env = a.seq_env[seq];
+    const float* x = a.qkv + (size_t)m * a.ld;
+    const float* ct = a.cos_tab + (size_t)pos * half;
+    const float* st = a.sin_tab + (size_t)pos * half;
+    const int blk = a.kv.block_table[(size_t)env * a.kv.bt_stride + (pos >> 4)];
+    T* kdst = (T*)a.kv.base + (size_t)blk * 2 * hkv * KV_BLOCK * hd + (size_t)(pos & 15) * hd;
+    T* vdst = kdst + (size_t)hkv * KV_BLOCK * hd;
+    T* q = (T*)a.Q + (size_t)m * a.ldq;
+    // rotated queries
+    for (int idx = threadIdx.x; idx < hq * half; idx += blockDim.x) {
+        const int h = idx / half, i = idx - h * half;
+        const float x1 = x[h * hd + i], x2 = x[h * hd + i + half];
+        float o1 = x1, o2 = x2;
+        if (a.use_rope) {
+            const float c = ct[i], sn = st[i];
+            o1 = x1 * c - x2 * sn;
+            o2 = x2 * c + x1 * sn;
+        }
+        st_elem<T>(q + h * hd + i, o1);
+        st_elem<T>(q + h * hd + i + half, o2);
+    }
+    // rotated keys
+    const float* xk = x + hq * hd;
+    for (int idx = threadIdx.x; idx < hkv * half; idx += blockDim.x) {
+        const int h = idx / half, i = idx - h * half;
+        const float x1 = xk[h * hd + i], x2 = xk[h * hd + i + half];
+        float o1 = x1, o2 = x2;
+        if (a.use_rope) {
+            const float c = ct[i], sn = st[i];
+            o1 = x1 * c - x2 * sn;
+            o2 = x2 * c + x1 * sn;
+        }
+        T* kd = kdst + (size_t)h * KV_BLOCK * hd;
+        st_elem<T>(kd + i, o1);
+        st_elem<T>(kd + i + half, o2);
+    }
+    // values
+    const float* xv = x + (hq + hkv) * hd;
+    for (int idx = threadIdx.x; idx < hkv * hd; idx += blockDim.x) {
+        const int h = idx / hd, i = idx - h * hd;
+        st_elem<T>(vdst + (size_t)h * KV_BLOCK * hd + i, xv[idx]);
+    }
+}
+
+void rope_kv_write(const RopeKVArgs& a, hipStream_t s) {
+    if (a.M <= 0) return;
+    if (a.bf16) hipLaunchKernelGGL(rope_kv_kernel<bf16_t>, dim3(a.M), dim3(256), 0, s, a);
+    else hipLaunchKernelGGL(rope_kv_kernel<float>, dim3(a.M), dim3(256), 0, s, a);
+}
+
+// ------------------------------------------------------------ embedding --
+template <typename T>
+__global__ __launch_bounds__(256) void embed_kernel(const T* E, int n_rows_e, int d, const int* ids,
+                                                    const int* src, int stride, int off, const int* dst_rows,
+                                                    float* X, int ldx)
+{
+    const int i = blockIdx.x;
+    const int id = ids[src ? src[i] : i * stride + off];
+    const int dst = dst_rows ? dst_rows[i] : i;
+    float* x = X + (size_t)dst * ldx;
+    if (id < 0 || id >= n_rows_e) {  // out-of-range ids embed as zero rows
+        for (int j = threadIdx.x; j < d; j += blockDim.x) x[j] = 0.f;
+        return;
+    }
+    const T* e = E + (size_t)id * d;
+    for (int j = threadIdx.x; j < d; j += blockDim.x) x[j] = ld_elem<T>(e + j);
+}
+
+void embed_rows(bool bf16, const void* E, int n_rows_e, int d, const int* ids, const int* src, int stride,
+                int off, const int* dst_rows, float* X, int ldx, int n, hipStream_t s) {
+    if (n <= 0) return;
+    if (bf16)
+        hipLaunchKernelGGL(embed_kernel<bf16_t>, dim3(n), dim3(256), 0, s, (const bf16_t*)E, n_rows_e, d,
+                           ids, src, stride, off, dst_rows, X, ldx);
+    else
+        hipLaunchKernelGGL(embed_kernel<float>, dim3(n), dim3(256), 0, s, (const float*)E, n_rows_e, d,
+                           ids, src, stride, off, dst_rows, X, ldx);
+}
+
+// ----------------------------------------------------------- patchify --
+template <typename T>
+__global__ void im2col_kernel(const float* img, long total, int cams, int H, int W, int P, T* out,
+                              int kpad)
+{
+    const int gw = W / P, np = (H / P) * gw;
+    const int kreal = P * P * 3;
+    for (long e = blockIdx.x * (long)blockDim.x + threadIdx.x; e < total;
+         e += (long)gridDim.x * blockDim.x) {
+        const long row = e / kpad;
+        const int k = (int)(e - row * kpad);
+        float v = 0.f;
+        if (k < kreal) {
+            const int dy = k / (3 * P), rem = k - dy * 3 * P, dx = rem / 3, c = rem - dx * 3;
+            const long env = row / ((long)cams * np);
+            const int p = (int)(row - env * cams * np);
+            const int cam = p / np, pp = p - cam * np;
+            const int py = pp / gw, px = pp - py * gw;
+            v = img[((((env * cams + cam) * H) + py * P + dy) * (long)W + px * P + dx) * 3 + c];
+        }
+        st_elem<T>(out + e, v);
+    }
+}
+
+void im2col(bool bf16, const float* img, int n, int cams, int H, int W, int P, void* out, int kpad,
+            hipStream_t s) {
+    const long total = (long)n * cams * (H / P) * (W / P) * kpad;
+    if (total <= 0) return;
+    const int blocks = (int)std::min<long>((total + 255) / 256, 65536);
+    if (bf16)
+        hipLaunchKernelGGL(im2col_kernel<bf16_t>, dim3(blocks), dim3(256), 0, s, img, total, cams, H,
+                           W, P, (bf16_t*)out, kpad);
+    else
+        hipLaunchKernelGGL(im2col_kernel<float>, dim3(blocks), dim3(256), 0, s, img, total, cams, H,
+                           W, P, (float*)out, kpad);
+}
+
+// --------------------------------------------------------- action head --
+template <typename TW>
+__global__ __launch_bounds__(256) void logits_kernel(LogitsArgs a)
+{
+    extern __shared__ float sh[];
+    float* hn = sh;              // [d]
+    float* lg = sh + a.d;        // [n_bins]
+    __shared__ float red[16];
+    const int i = blockIdx.x;
+    const int src = a.rows ? a.rows[i] : i;
+    const float* x = a.X + (size_t)src * a.ldx;
+    const float rs = row_rstd(x, a.d, a.eps, red);
+    for (int j = threadIdx.x; j < a.d; j += blockDim.x) hn[j] = x[j] * rs;
+    __syncthreads();
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, nw = blockDim.x >> 6;
+    const TW* W = (const TW*)a.W;
+    for (int b = wave; b < a.n_bins; b += nw) {
+        float dot = 0.f;
+        for (int j = lane * 8; j < a.d; j += 512) {
+            float w[8];
+            load8v<TW>(W + (size_t)b * a.d + j, w);
+#pragma unroll
+            for (int u = 0; u < 8; ++u) dot = fmaf(w[u], hn[j + u], dot);
+        }
+        dot = wave_sum(dot);
+        if (lane == 0) lg[b] = dot;
+    }
+    __syncthreads();
+    if (wave == 0) {
+        // argmax, ties to the lowest index
+        float bv = -INFINITY;
+        int bi = 0x7fffffff;
+        for (int b = lane; b < a.n_bins; b += 64) {
+            const float v = lg[b];
+            if (v > bv || (v == bv && b < bi)) { bv = v; bi = b; }
+        }
+#pragma unroll
+        for (int off = 32; off > 0; off >>= 1) {
+            const float ov = __shfl_xor(bv, off, 64);
+            const int oi = __shfl_xor(bi, off, 64);
+            if (ov > bv || (ov == bv && oi < bi)) { bv = ov; bi = oi; }
+        }
+        float sv = -INFINITY;
+        for (int b = lane; b < a.n_bins; b += 64)
+            if (b != bi) sv = fmaxf(sv, lg[b]);
+        sv = wave_max(sv);
+        if (lane == 0) {
+            const int o = i * a.ntok + a.col;
+            a.tokens[o] = bi;
+            if (a.actions) a.actions[o] = -1.0f + (2.0f * (float)bi + 1.0f) / (float)a.n_bins;
+            if (a.margins) a.margins[o] = bv - sv;
+        }
+    }
+}
+
+void action_logits(const LogitsArgs& a, hipStream_t s) {
+    if (a.n <= 0) return;
+    const size_t shm = (size_t)(a.d + a.n_bins) * sizeof(float);
+    if (a.bf16) hipLaunchKernelGGL(logits_kernel<bf16_t>, dim3(a.n), dim3(256), shm, s, a);
+    else hipLaunchKernelGGL(logits_kernel<float>, dim3(a.n), dim3(256), shm, s, a);
+}
+
+// ---------------------------------------------------- last prefix row --
+__global__ __launch_bounds__(256) void gather_last_kernel(const float* X, int ldx, const int* seq_env,
+                                                          const int* last_row, int d, float eps,
+                                                          float* h_pre, float* h_norm)
+{
+    __shared__ float red[16];
+    const int i = blockIdx.x;
+    const float* x = X + (size_t)last_row[i] * ldx;
+    const int env = seq_env[i];
+    const float rs = row_rstd(x, d, eps, red);
+    for (int j = threadIdx.x; j < d; j += blockDim.x) {
+        h_pre[(size_t)env * d + j] = x[j];
+        h_norm[(size_t)env * d + j] = x[j] * rs;
+    }
+}
+
+void gather_last(const float* X, int ldx, const int* seq_env, const int* last_row, int n, int d,
+                 float eps, float* h_pre, float* h_norm, hipStream_t s) {
+    if (n <= 0) return;
+    hipLaunchKernelGGL(gather_last_kernel, dim3(n), dim3(256), 0, s, X, ldx, seq_env, last_row, d,
+                       eps, h_pre, h_norm);
+}
+
+// ------------------------------------------------------- small linear --
+template <typename T>
+__global__ void small_linear_kernel(const float* in, int R, int K, const T* W, int N, float* out,
+                                    int silu_input)
+{
+    const int idx = blockIdx.x * blockDim.x + threadIdx.x;
+    if (idx >= R * N) return;
+    const int r = idx / N, n = idx - r * N;
+    float acc = 0.f;
+    for (int k = 0; k < K; ++k) {
+        float v = in[(size_t)r * K + k];
+        if (silu_input) v = v / (1.0f + expf(-v));
+        acc = fmaf(v, ld_elem<T>(W + (size_t)n * K + k), acc);
+    }
+    out[idx] = acc;
+}
+
+void small_linear(bool bf16, const float* in, int R, int K, const void* W, int N, float* out,
+                  bool silu_input, hipStream_t s) {
+    const int total = R * N;
+    if (total <= 0) return;
+    if (bf16)
+        hipLaunchKernelGGL(small_linear_kernel<bf16_t>, dim3((total + 255) / 256), dim3(256), 0, s, in,
+                           R, K, (const bf16_t*)W, N, out, (int)silu_input);
+    else
+        hipLaunchKernelGGL(small_linear_kernel<float>, dim3((total + 255) / 256), dim3(256), 0, s, in,
+                           R, K, (const float*)W, N, out, (int)silu_input);
+}
+
+// ------------------------------------------------------------- flow --
+template <typename T>
+__global__ __launch_bounds__(256) void flow_in_kernel(const float* x, int adim, const T* W_ain,
+                                                      const float* tvec, int d, float* H, int ldh)
+{
+    const int r = blockIdx.x;
+    const float* xr = x + (size_t)r * adim;
+    for (int o = threadIdx.x; o < d; o += blockDim.x) {
+        float acc = 0.f;
+        for (int j = 0; j < adim; ++j) acc = fmaf(ld_elem<T>(W_ain + (size_t)o * adim + j), xr[j], acc);
+        H[(size_t)r * ldh + o] = acc + tvec[o];
+    }
+}
+
+void flow_in(bool bf16, const float* x, int rows, int adim, const void* W_ain, const float* tvec,
+             int d, float* H, int ldh, hipStream_t s) {
+    if (rows <= 0) return;
+    if (bf16)
+        hipLaunchKernelGGL(flow_in_kernel<bf16_t>, dim3(rows), dim3(256), 0, s, x, adim,
+                           (const bf16_t*)W_ain, tvec, d, H, ldh);
+    else
+        hipLaunchKernelGGL(flow_in_kernel<float>, dim3(rows), dim3(256), 0, s, x, adim,
+                           (const float*)W_ain, tvec, d, H, ldh);
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void flow_out_kernel(const float* H, int ldh, int d, const T* W_aout,
+                                                       int adim, float eps, float n_steps, float* x,
+                                                       float* v_out)
+{
+    extern __shared__ float sh[];
+    float* hn = sh;          // [d]
+    float* vv = sh + d;      // [adim]
+    __shared__ float red[16];
+    const int r = blockIdx.x;
+    const float* h = H + (size_t)r * ldh;
+    const float rs = row_rstd(h, d, eps, red);
+    for (int j = threadIdx.x; j < d; j += blockDim.x) hn[j] = h[j] * rs;
+    __syncthreads();
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, nw = blockDim.x >> 6;
+    for (int c = wave; c < adim; c += nw) {
+        float dot = 0.f;
+        for (int j = lane; j < d; j += 64) dot = fmaf(ld_elem<T>(W_aout + (size_t)c * d + j), hn[j], dot);
+        dot = wave_sum(dot);
+        if (lane == 0) vv[c] = dot;
+    }
+    __syncthreads();
+    if (threadIdx.x < adim) {
+        const int c = threadIdx.x;
+        const float v = vv[c];
+        x[(size_t)r * adim + c] -= v / n_steps;
+        if (v_out) v_out[(size_t)r * adim + c] = v;
+    }
+}
+
+void flow_out(bool bf16, const float* H, int ldh, int rows, int d, const void* W_aout, int adim,
+              float eps, float n_steps, float* x, float* v_out, hipStream_t s) {
+    if (rows <= 0) return;
+    const size_t shm = (size_t)(d + adim) * sizeof(float);
+    if (bf16)
+        hipLaunchKernelGGL(flow_out_kernel<bf16_t>, dim3(rows), dim3(256), shm, s, H, ldh, d,
+                           (const bf16_t*)W_aout, adim, eps, n_steps, x, v_out);
+    else
+        hipLaunchKernelGGL(flow_out_kernel<float>, dim3(rows), dim3(256), shm, s, H, ldh, d,
+                           (const float*)W_aout, adim, eps, n_steps, x, v_out);
+}
+
+__global__ void copy_f32_kernel(const float* src, float* dst, size_t n) {
+    for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x)
+        dst[i] = src[i];
+}
+
+void copy_f32(const float* src, float* dst, size_t n, hipStream_t s) {
+    if (n == 0) return;
+    const int blocks = (int)std::min<size_t>((n + 255) / 256, 4096);
+    hipLaunchKernelGGL(copy_f32_kernel, dim3(blocks), dim3(256), 0, s, src, dst, n);
+}
+
+}  // namespace ebrl

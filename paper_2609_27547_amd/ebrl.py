@@ -1,0 +1,264 @@
+"""Thin Python binding of the C ABI in include/ebrl.h (argument marshalling only).
+
+Every step of the policy forward runs in libebrl.so's HIP kernels; this
+module only passes device pointers (from torch tensors), host id arrays and
+the stream handle.  PyTorch supplies device memory and streams.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libebrl.so")
+
+EBRL_OK = 0
+ERRORS = {-1: "EBRL_E_INVALID", -2: "EBRL_E_OOM", -3: "EBRL_E_HIP", -4: "EBRL_E_STATE",
+          -5: "EBRL_E_UNSUPPORTED"}
+DTYPE_FP32, DTYPE_BF16 = 0, 1
+STATE_H_LAST_PRE, STATE_H_LAST, STATE_K, STATE_V, STATE_FLOW_V0, STATE_PREFIX_LEN = range(6)
+K_GEMM, K_GEMM_SKINNY, K_ATTN_PREFILL, K_ATTN_DECODE, K_OTHER = range(5)
+KERNEL_CLASSES = {K_GEMM: "gemm", K_GEMM_SKINNY: "gemm_skinny", K_ATTN_PREFILL: "attn_prefill",
+                  K_ATTN_DECODE: "attn_decode", K_OTHER: "other"}
+
+_I32 = ctypes.c_int32
+
+
+class Config(ctypes.Structure):
+    _fields_ = [(n, _I32) for n in (
+        "dtype", "n_cams", "img", "patch", "vit_layers", "vit_d", "vit_heads", "vit_mlp",
+        "layers", "d", "q_heads", "kv_heads", "head_dim", "mlp", "vocab", "n_lang",
+        "action_logits", "n_action_tokens", "n_bins",
+        "exp_layers", "exp_d", "exp_heads", "exp_mlp", "chunk", "adim", "n_steps",
+        "max_envs", "max_seq")] + [("kv_budget_bytes", ctypes.c_int64), ("init_std", ctypes.c_double)]
+
+    def as_dict(self):
+        return {n: getattr(self, n) for n, _ in self._fields_}
+
+
+class ObsBatch(ctypes.Structure):
+    _fields_ = [("images", ctypes.c_void_p), ("lang_ids", ctypes.c_void_p),
+                ("lang_len", ctypes.c_void_p), ("lang_stride", _I32)]
+
+
+class EbrlError(RuntimeError):
+    def __init__(self, code, msg):
+        super().__init__(f"{ERRORS.get(code, code)}: {msg}")
+        self.code = code
+
+
+_LIB = None
+
+EXPORTED = [
+    "ebrl_config_preset", "ebrl_policy_create", "ebrl_policy_destroy",
+    "ebrl_stream_create_cu_masked", "ebrl_stream_destroy", "ebrl_policy_bind_stream",
+    "ebrl_prefill", "ebrl_decode_actions", "ebrl_flow_denoise", "ebrl_last_error",
+    "ebrl_read_state", "ebrl_generate_weight_host", "ebrl_read_weight", "ebrl_write_weight",
+    "ebrl_profile_enable", "ebrl_profile_read", "ebrl_op_gemm",
+]
+
+
+def lib():
+    """Load libebrl.so; raises if it has not been built (there is no fallback)."""
+    global _LIB
+    if _LIB is not None:
+        return _LIB
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is missing: build it with "
+                          "`python -c 'import __graft_entry__ as g; g.build()'`")
+    L = ctypes.CDLL(LIB_PATH)
+    vp, i32, i64, u32, u64 = ctypes.c_void_p, _I32, ctypes.c_int64, ctypes.c_uint32, ctypes.c_uint64
+    pI32 = ctypes.POINTER(_I32)
+    sig = {
+        "ebrl_config_preset": (i32, [i32, ctypes.POINTER(Config)]),
+        "ebrl_policy_create": (i32, [ctypes.POINTER(Config), u64, ctypes.POINTER(vp)]),
+        "ebrl_policy_destroy": (None, [vp]),
+        "ebrl_stream_create_cu_masked": (i32, [i32, ctypes.POINTER(u32), u32, ctypes.POINTER(vp)]),
+        "ebrl_stream_destroy": (i32, [vp]),
+        "ebrl_policy_bind_stream": (i32, [vp, vp]),
+        "ebrl_prefill": (i32, [vp, ctypes.POINTER(ObsBatch), pI32, i32]),
+        "ebrl_decode_actions": (i32, [vp, pI32, i32, vp, vp, vp]),
+        "ebrl_flow_denoise": (i32, [vp, pI32, i32, vp, vp]),
+        "ebrl_last_error": (ctypes.c_char_p, [vp]),
+        "ebrl_read_state": (i32, [vp, i32, i32, i32, vp, i64]),
+        "ebrl_generate_weight_host": (i32, [u64, u32, i64, ctypes.c_double, i32, vp]),
+        "ebrl_read_weight": (i32, [vp, u32, vp, i64]),
+        "ebrl_write_weight": (i32, [vp, u32, vp, i64]),
+        "ebrl_profile_enable": (i32, [vp, i32]),
+        "ebrl_profile_read": (i32, [vp, i32, ctypes.POINTER(i64), ctypes.POINTER(ctypes.c_double),
+                                    ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double), i32]),
+        "ebrl_op_gemm": (i32, [i32, vp, vp, vp, i32, i32, i32, vp]),
+    }
+    for name, (res, args) in sig.items():
+        f = getattr(L, name)
+        f.restype = res
+        f.argtypes = args
+    _LIB = L
+    return L
+
+
+def preset(n: int) -> Config:
+    c = Config()
+    rc = lib().ebrl_config_preset(n, ctypes.byref(c))
+    if rc != EBRL_OK:
+        raise EbrlError(rc, f"unknown preset {n}")
+    return c
+
+
+def _ids(env_ids) -> ctypes.Array:
+    a = np.ascontiguousarray(np.asarray(env_ids, dtype=np.int32))
+    return a, a.ctypes.data_as(ctypes.POINTER(_I32))
+
+
+def _ptr(t) -> Optional[int]:
+    return None if t is None else int(t.data_ptr())
+
+
+def generate_weight_host(seed: int, tensor_id: int, count: int, std: float, bf16: bool) -> np.ndarray:
+    out = np.empty(count, dtype=np.uint16 if bf16 else np.float32)
+    rc = lib().ebrl_generate_weight_host(seed, tensor_id, count, std, int(bf16), out.ctypes.data)
+    if rc != EBRL_OK:
+        raise EbrlError(rc, "generate_weight_host")
+    return out
+
+
+def op_gemm(A, B, C, stream=None) -> None:
+    """C = A B^T through the library's GEMM kernel (torch device tensors)."""
+    import torch
+    dt = DTYPE_BF16 if A.dtype == torch.bfloat16 else DTYPE_FP32
+    M, K = A.shape
+    N = B.shape[0]
+    s = stream if stream is not None else torch.cuda.current_stream().cuda_stream
+    rc = lib().ebrl_op_gemm(dt, A.data_ptr(), B.data_ptr(), C.data_ptr(), M, N, K, s)
+    if rc != EBRL_OK:
+        raise EbrlError(rc, "ebrl_op_gemm")
+
+
+def create_cu_masked_stream(device: int, mask_words: Sequence[int]) -> int:
+    arr = (ctypes.c_uint32 * len(mask_words))(*[int(w) & 0xFFFFFFFF for w in mask_words])
+    out = ctypes.c_void_p()
+    rc = lib().ebrl_stream_create_cu_masked(device, arr, len(mask_words), ctypes.byref(out))
+    if rc != EBRL_OK:
+        raise EbrlError(rc, lib().ebrl_last_error(None).decode())
+    return out.value
+
+
+def destroy_stream(s: int) -> None:
+    lib().ebrl_stream_destroy(s)
+
+
+class Policy:
+    """One policy on the current device; calls enqueue on the bound stream."""
+
+    def __init__(self, config, seed: int = 0, stream=None, **overrides):
+        import torch
+        cfg = preset(config) if isinstance(config, int) else config
+        for k, v in overrides.items():
+            setattr(cfg, k, v)
+        self.cfg = cfg
+        self.seed = seed
+        h = ctypes.c_void_p()
+        rc = lib().ebrl_policy_create(ctypes.byref(cfg), seed, ctypes.byref(h))
+        if rc != EBRL_OK:
+            raise EbrlError(rc, lib().ebrl_last_error(None).decode())
+        self.h = h.value
+        self.torch = torch
+        self.bind_stream(stream if stream is not None else torch.cuda.current_stream().cuda_stream)
+
+    # lifecycle -------------------------------------------------------------
+    def close(self):
+        if getattr(self, "h", None):
+            lib().ebrl_policy_destroy(self.h)
+            self.h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def _check(self, rc, what):
+        if rc != EBRL_OK:
+            raise EbrlError(rc, f"{what}: {lib().ebrl_last_error(self.h).decode()}")
+
+    def bind_stream(self, stream) -> None:
+        self.stream = int(stream or 0)
+        self._check(lib().ebrl_policy_bind_stream(self.h, self.stream or None), "bind_stream")
+
+    @property
+    def bf16(self) -> bool:
+        return self.cfg.dtype == DTYPE_BF16
+
+    # calls -----------------------------------------------------------------
+    def prefill(self, env_ids, images=None, lang_ids=None, lang_len=None) -> None:
+        ids, pids = _ids(env_ids)
+        ob = ObsBatch()
+        ob.images = _ptr(images)
+        ob.lang_ids = _ptr(lang_ids)
+        ob.lang_stride = int(lang_ids.shape[1]) if lang_ids is not None else 0
+        ll = None
+        if lang_len is not None:
+            ll = np.ascontiguousarray(np.asarray(lang_len, dtype=np.int32))
+            ob.lang_len = ll.ctypes.data
+        self._keep = (ids, ll, images, lang_ids)
+        self._check(lib().ebrl_prefill(self.h, ctypes.byref(ob), pids, len(ids)), "prefill")
+
+    def decode_actions(self, env_ids, tokens=None, actions=None, margins=None, with_margin=True):
+        torch = self.torch
+        ids, pids = _ids(env_ids)
+        n, nt = len(ids), self.cfg.n_action_tokens
+        dev = torch.device("cuda", torch.cuda.current_device())
+        if tokens is None:
+            tokens = torch.empty((n, nt), dtype=torch.int32, device=dev)
+        if actions is None:
+            actions = torch.empty((n, nt), dtype=torch.float32, device=dev)
+        if margins is None and with_margin:
+            margins = torch.empty((n, nt), dtype=torch.float32, device=dev)
+        self._check(lib().ebrl_decode_actions(self.h, pids, n, _ptr(tokens), _ptr(actions), _ptr(margins)),
+                    "decode_actions")
+        return tokens, actions, margins
+
+    def flow_denoise(self, env_ids, noise, out=None):
+        torch = self.torch
+        ids, pids = _ids(env_ids)
+        if out is None:
+            out = torch.empty_like(noise)
+        self._check(lib().ebrl_flow_denoise(self.h, pids, len(ids), _ptr(noise), _ptr(out)), "flow_denoise")
+        return out
+
+    # inspection ------------------------------------------------------------
+    def read_state(self, what: int, env_id: int, layer: int = 0) -> np.ndarray:
+        c = self.cfg
+        if what in (STATE_H_LAST_PRE, STATE_H_LAST):
+            out = np.empty(c.d, dtype=np.float32)
+        elif what == STATE_PREFIX_LEN:
+            out = np.empty(1, dtype=np.int32)
+        elif what == STATE_FLOW_V0:
+            out = np.empty((c.chunk, c.adim), dtype=np.float32)
+        else:
+            T = int(self.read_state(STATE_PREFIX_LEN, env_id)[0])
+            out = np.empty((T, c.kv_heads, c.head_dim), dtype=np.uint16 if self.bf16 else np.float32)
+        self._check(lib().ebrl_read_state(self.h, what, env_id, layer, out.ctypes.data, out.nbytes), "read_state")
+        return out
+
+    def read_weight(self, tensor_id: int, shape) -> np.ndarray:
+        out = np.empty(shape, dtype=np.uint16 if self.bf16 else np.float32)
+        self._check(lib().ebrl_read_weight(self.h, tensor_id, out.ctypes.data, out.nbytes), "read_weight")
+        return out
+
+    def write_weight(self, tensor_id: int, values: np.ndarray) -> None:
+        a = np.ascontiguousarray(values, dtype=np.uint16 if self.bf16 else np.float32)
+        self._check(lib().ebrl_write_weight(self.h, tensor_id, a.ctypes.data, a.nbytes), "write_weight")
+
+    def profile_enable(self, on: bool = True) -> None:
+        self._check(lib().ebrl_profile_enable(self.h, int(on)), "profile_enable")
+
+    def profile_read(self, cls: int, reset: bool = False) -> dict:
+        n = ctypes.c_int64()
+        ms, fl, by = ctypes.c_double(), ctypes.c_double(), ctypes.c_double()
+        self._check(lib().ebrl_profile_read(self.h, cls, ctypes.byref(n), ctypes.byref(ms), ctypes.byref(fl),
+                                            ctypes.byref(by), int(reset)), "profile_read")
+        return {"launches": n.value, "ms": ms.value, "flop": fl.value, "bytes": by.value}
