@@ -191,8 +191,9 @@ int ebrl_read_weight(ebrl_policy* p, uint32_t tensor_id, void* out, int64_t byte
 int ebrl_write_weight(ebrl_policy* p, uint32_t tensor_id, const void* in, int64_t bytes);
 
 /* Per-kernel timing for roofline reports.  While enabled, every launch of
- * the kernel classes below is bracketed by HIP events on the bound stream
- * and its algorithmic FLOP and HBM bytes are accumulated. */
+ * a kernel class whose bit (1 << class) is set in class_mask is bracketed by
+ * HIP events on the bound stream, and its algorithmic FLOP and HBM bytes are
+ * accumulated.  class_mask = 0 disables timing. */
 enum {
     EBRL_K_GEMM = 0,            /* bf16/fp32 GEMMs of prefill, ViT and flow expert (M > 256) */
     EBRL_K_GEMM_SKINNY = 1,     /* decode GEMMs (M <= 256) */
@@ -201,7 +202,7 @@ enum {
     EBRL_K_OTHER = 4,           /* norms, rotary/KV write, gathers, logits, flow update */
     EBRL_K_COUNT = 5
 };
-int ebrl_profile_enable(ebrl_policy* p, int32_t on);
+int ebrl_profile_enable(ebrl_policy* p, int32_t class_mask);
 /* Totals since enable (and resets them when reset != 0).  Synchronises. */
 int ebrl_profile_read(ebrl_policy* p, int32_t kernel_class, int64_t* launches, double* total_ms,
                       double* flop, double* bytes, int32_t reset);

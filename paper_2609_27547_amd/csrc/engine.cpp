@@ -115,6 +115,7 @@ struct ebrl_policy {
 
     // profiling
     bool prof = false;
+    int prof_mask = 0;
     std::vector<ProfRec> recs;
     std::vector<hipEvent_t> ev_pool;
     int64_t p_launch[EBRL_K_COUNT] = {};
@@ -190,7 +191,7 @@ hipEvent_t get_event(ebrl_policy* p) {
 }
 
 void prof_begin(ebrl_policy* p, int cls) {
-    if (!p->prof) return;
+    if (!p->prof || !(p->prof_mask & (1 << cls))) return;
     p->cur_cls = cls;
     p->cur_a = get_event(p);
     (void)hipEventRecord(p->cur_a, p->stream);
@@ -432,6 +433,7 @@ struct BlockCall {
     bool use_rope = true;
     // attention
     bool decode = false;
+    double attn_flop = 0, attn_bytes = 0;  // algorithmic work of the attention launch
     AttnPrefillArgs pre;
     AttnDecodeArgs dec;
 };
@@ -458,13 +460,13 @@ int run_block(ebrl_policy* p, BlockCall& b) {
         b.dec.q_heads = s.hq; b.dec.kv = b.kv; b.dec.part = p->part;
         prof_begin(p, EBRL_K_ATTN_DECODE);
         attn_decode(b.dec, p->stream);
-        prof_end(p, 0, 0);  // bytes filled by the caller's accounting
+        prof_end(p, b.attn_flop, b.attn_bytes);
     } else {
         b.pre.bf16 = p->bf16; b.pre.Q = p->Qb; b.pre.ldq = qn; b.pre.O = p->Ob; b.pre.ldo = qn;
         b.pre.q_heads = s.hq; b.pre.kv = b.kv;
         prof_begin(p, EBRL_K_ATTN_PREFILL);
         attn_prefill(b.pre, p->stream);
-        prof_end(p, 0, 0);
+        prof_end(p, b.attn_flop, b.attn_bytes);
     }
     g = GemmArgs();
     g.A = p->Ob; g.lda = qn; g.B = b.w->o; g.ldb = qn; g.M = b.rows; g.N = s.d; g.K = qn;
@@ -910,6 +912,7 @@ int ebrl_prefill(ebrl_policy* p, const ebrl_obs_batch* obs, const int32_t* env_i
                 b.pre.q_pos0 = md + o_vzero; b.pre.kv_len = md + o_vlen; b.pre.tile_seq = md + o_vtseq;
                 b.pre.tile_q0 = md + o_vtq0; b.pre.n_tiles = (int)v_tseq.size(); b.pre.causal = false;
                 b.pre.max_kv_len = pv;
+                b.attn_flop = 4.0 * p->vit.hd * p->vit.hq * (double)n * pv * pv;
                 if ((rc = run_block(p, b))) return rc;
             }
             prof_begin(p, EBRL_K_OTHER);
@@ -933,6 +936,8 @@ int ebrl_prefill(ebrl_policy* p, const ebrl_obs_batch* obs, const int32_t* env_i
     }
     // ---- decoder
     const int maxT = *std::max_element(T.begin(), T.end());
+    double causal_pairs = 0, kv_rows = 0;
+    for (int i = 0; i < n; ++i) { causal_pairs += 0.5 * T[i] * (T[i] + 1.0); kv_rows += T[i]; }
     for (int l = 0; l < c.layers; ++l) {
         BlockCall b;
         b.R = p->X; b.rows = M; b.sd = &p->dec; b.w = &p->L_dec[l]; b.kv = dec_kv(p, l);
@@ -940,6 +945,8 @@ int ebrl_prefill(ebrl_policy* p, const ebrl_obs_batch* obs, const int32_t* env_i
         b.pre.seq_env = md + o_env; b.pre.q_off = md + o_off; b.pre.q_len = md + o_len; b.pre.q_pos0 = md + o_pos0;
         b.pre.kv_len = md + o_len; b.pre.tile_seq = md + o_tseq; b.pre.tile_q0 = md + o_tq0;
         b.pre.n_tiles = (int)tiles.size(); b.pre.causal = true; b.pre.max_kv_len = maxT;
+        b.attn_flop = 4.0 * c.head_dim * c.q_heads * causal_pairs;
+        b.attn_bytes = 2.0 * kv_rows * c.kv_heads * c.head_dim * p->esz * 2.0;  // Q/O + K/V once
         if ((rc = run_block(p, b))) return rc;
     }
     prof_begin(p, EBRL_K_OTHER);
@@ -997,15 +1004,9 @@ int ebrl_decode_actions(ebrl_policy* p, const int32_t* env_ids, int32_t n, int32
             b.decode = true;
             b.dec.seq_env = md + o_env; b.dec.kv_len = md + o_kvl + (size_t)(k - 1) * n; b.dec.n = n;
             b.dec.max_splits = max_splits;
-            if (p->prof) {
-                // attention bytes are known here
-                if ((rc = run_block(p, b))) return rc;
-                // patch the last attention record with its algorithmic bytes
-                for (auto it = p->recs.rbegin(); it != p->recs.rend(); ++it)
-                    if (it->cls == EBRL_K_ATTN_DECODE) { it->bytes = kv_bytes; break; }
-            } else if ((rc = run_block(p, b))) {
-                return rc;
-            }
+            b.attn_bytes = kv_bytes;
+            b.attn_flop = kv_bytes / p->esz / (2.0 * c.kv_heads * c.head_dim) * 4.0 * c.q_heads * c.head_dim;
+            if ((rc = run_block(p, b))) return rc;
         }
         la.X = p->X; la.rows = nullptr; la.col = k;
         prof_begin(p, EBRL_K_OTHER);
@@ -1061,6 +1062,8 @@ int ebrl_flow_denoise(ebrl_policy* p, const int32_t* env_ids, int32_t n, const f
             b.pre.q_pos0 = md + o_pos0; b.pre.kv_len = md + o_kvl; b.pre.tile_seq = md + o_tseq;
             b.pre.tile_q0 = md + o_tq0; b.pre.n_tiles = (int)tseq.size(); b.pre.causal = false;
             b.pre.max_kv_len = maxkv;
+            b.attn_flop = 0;
+            for (int i = 0; i < n; ++i) b.attn_flop += 4.0 * c.head_dim * p->exp.hq * (double)c.chunk * kv_len[i];
             if ((rc = run_block(p, b))) return rc;
         }
         prof_begin(p, EBRL_K_OTHER);
@@ -1165,11 +1168,12 @@ int ebrl_write_weight(ebrl_policy* p, uint32_t tensor_id, const void* in, int64_
     return weight_io(p, tensor_id, const_cast<void*>(in), bytes, true);
 }
 
-int ebrl_profile_enable(ebrl_policy* p, int32_t on) {
+int ebrl_profile_enable(ebrl_policy* p, int32_t class_mask) {
     int rc = check_ready(p);
     if (rc) return rc;
-    if (!on) prof_collect(p);
-    p->prof = on != 0;
+    if (!class_mask) prof_collect(p);
+    p->prof = class_mask != 0;
+    p->prof_mask = class_mask;
     return EBRL_OK;
 }
 

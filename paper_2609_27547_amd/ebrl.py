@@ -253,8 +253,11 @@ class Policy:
         a = np.ascontiguousarray(values, dtype=np.uint16 if self.bf16 else np.float32)
         self._check(lib().ebrl_write_weight(self.h, tensor_id, a.ctypes.data, a.nbytes), "write_weight")
 
-    def profile_enable(self, on: bool = True) -> None:
-        self._check(lib().ebrl_profile_enable(self.h, int(on)), "profile_enable")
+    def profile_enable(self, classes=(K_GEMM, K_GEMM_SKINNY, K_ATTN_PREFILL, K_ATTN_DECODE, K_OTHER)) -> None:
+        mask = 0
+        for c in classes:
+            mask |= 1 << c
+        self._check(lib().ebrl_profile_enable(self.h, mask), "profile_enable")
 
     def profile_read(self, cls: int, reset: bool = False) -> dict:
         n = ctypes.c_int64()
