@@ -159,7 +159,7 @@ def main():
     achieved = gemm["flop"] / (gemm["ms"] * 1e9) if gemm["ms"] else 0.0
     roofline = {"bound": "mfma", "achieved": round(achieved, 1), "peak": peak, "unit": "TFLOP/s",
                 "frac": round(achieved / peak, 4), "traffic": None,
-                "kernel": "gemm_bf16_kernel (prefill projections, M > 256)",
+                "kernel": "gemm_bf16_big_kernel (prefill projections, M >= 256)",
                 "launches": gemm["launches"], "avg_launch_us": round(1000 * gemm["ms"] / max(1, gemm["launches"]), 2),
                 "flop_per_launch": round(gemm["flop"] / max(1, gemm["launches"])),
                 "share_of_step": round(gemm["ms"] / gpu_ms, 3) if gpu_ms else None}

@@ -412,7 +412,7 @@ int run_gemm(ebrl_policy* p, GemmArgs a) {
     a.bf16 = p->bf16;
     a.ws = p->ws;
     a.ws_floats = p->ws_floats;
-    const int cls = a.M > 256 ? EBRL_K_GEMM : EBRL_K_GEMM_SKINNY;
+    const int cls = a.M >= 256 ? EBRL_K_GEMM : EBRL_K_GEMM_SKINNY;
     prof_begin(p, cls);
     ebrl::gemm(a, p->stream);
     const double flop = 2.0 * a.M * (double)a.N * a.K;

@@ -210,6 +210,160 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(
     }
 }
 
+
+// ------------------------------------------------ bf16 MFMA GEMM, large M --
+// 256-row macro tiles, 4 waves in 2 x 2, each wave a 128 x (BN/2) tile.
+// Operands go global -> LDS with global_load_lds_dwordx4 (no VGPR staging):
+// a wave instruction writes 64 lanes x 16 bytes contiguously, so the tile is
+// stored as 16-byte chunks, chunk (row, c) of a 64-element row at position
+// row * 8 + (c ^ (row & 7)); the XOR makes the MFMA fragment reads of 8
+// consecutive rows hit 8 different bank groups.  Two LDS stages: the loads of
+// K tile t+1 are in flight while tile t is multiplied.  Block ids are
+// remapped so that consecutive tiles of one row band run on the same XCD
+// (the dispatcher deals block ids round-robin over the 8 XCDs).
+typedef __attribute__((address_space(3))) void* lds_ptr_t;
+
+EBRL_DEV void wait_vm_all() { __builtin_amdgcn_s_waitcnt(0); }
+
+template <int ROWS, int NW>
+EBRL_DEV void load_tile_lds(const bf16_t* __restrict__ G, int ld, int row0_g, int rows_valid, int k0,
+                            bf16_t* lds_tile, int wave, int lane) {
+    // each of the NW waves fills ROWS/NW rows, 8 rows per instruction
+#pragma unroll
+    for (int j = 0; j < ROWS / (8 * NW); ++j) {
+        const int r0 = wave * (ROWS / NW) + j * 8;
+        const int row = r0 + (lane >> 3);
+        const int c = (lane & 7) ^ (row & 7);
+        const int gr = min(row0_g + row, rows_valid - 1);
+        const bf16_t* src = G + (size_t)gr * ld + k0 + c * 8;
+        __builtin_amdgcn_global_load_lds((const void*)src, (lds_ptr_t)(lds_tile + r0 * 64), 16, 0, 0);
+    }
+}
+
+EBRL_DEV bf16x8 lds_frag(const bf16_t* tile, int row, int c) {
+    return *reinterpret_cast<const bf16x8*>(tile + row * 64 + ((c ^ (row & 7)) << 3));
+}
+
+template <int BN, int WM, int WN, bool PAIRED, bool SPLIT, class Epi>
+__global__ __launch_bounds__(64 * WM * WN, 1) void gemm_bf16_big_kernel(
+    const bf16_t* __restrict__ A, int lda, const bf16_t* __restrict__ B, int ldb, int M, int N, int K,
+    int k_per_split, float* __restrict__ ws, Epi epi)
+{
+    constexpr int BM = 256;
+    constexpr int NW = WM * WN;
+    constexpr int WTM = BM / WM, WTN = BN / WN;
+    constexpr int TM = WTM / 16, TN = WTN / 16;
+    static_assert(!PAIRED || (TN % 2 == 0), "paired epilogue needs tile pairs");
+    // one __shared__ object per stage, so that the compiler can tell the
+    // stage being read from the stage the DMA is filling
+    __shared__ __attribute__((aligned(1024))) bf16_t sA0[BM * 64];
+    __shared__ __attribute__((aligned(1024))) bf16_t sA1[BM * 64];
+    __shared__ __attribute__((aligned(1024))) bf16_t sB0[BN * 64];
+    __shared__ __attribute__((aligned(1024))) bf16_t sB1[BN * 64];
+
+    const int tiles_m = (M + BM - 1) / BM, tiles_n = (N + BN - 1) / BN;
+    int bid = blockIdx.x;
+    const int nb = gridDim.x;
+    if ((nb & 7) == 0) bid = (bid & 7) * (nb >> 3) + (bid >> 3);
+    constexpr int G = 4;  // row tiles per group
+    const int group = G * tiles_n;
+    const int first_m = (bid / group) * G;
+    const int gsz = min(tiles_m - first_m, G);
+    const int within = bid - (bid / group) * group;
+    const int tm_idx = first_m + within % gsz, tn_idx = within / gsz;
+    const int m0 = tm_idx * BM, n0 = tn_idx * BN;
+
+    const int k_begin = blockIdx.y * k_per_split;
+    const int k_end = min(K, k_begin + k_per_split);
+    const int nk = (k_end - k_begin) / 64;
+
+    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+    const int wm = wave / WN, wn = wave - (wave / WN) * WN;
+    const int r = lane & 15, g = lane >> 4;
+
+    f32x4 acc[TM][TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    // All fragment reads of the K tile are issued first, so the second
+    // half's reads overlap the first half's MFMAs.
+    auto compute = [&](const bf16_t* ta, const bf16_t* tb) {
+        bf16x8 wa[2][TN], xb[2][TM];
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) {
+#pragma unroll
+            for (int j = 0; j < TN; ++j) wa[ks][j] = lds_frag(tb, wn * WTN + j * 16 + r, ks * 4 + g);
+#pragma unroll
+            for (int i = 0; i < TM; ++i) xb[ks][i] = lds_frag(ta, wm * WTM + i * 16 + r, ks * 4 + g);
+        }
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+#pragma unroll
+                for (int j = 0; j < TN; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wa[ks][j], xb[ks][i], acc[i][j], 0, 0, 0);
+    };
+
+    if (nk > 0) {
+        load_tile_lds<BM, NW>(A, lda, m0, M, k_begin, sA0, wave, lane);
+        load_tile_lds<BN, NW>(B, ldb, n0, N, k_begin, sB0, wave, lane);
+        wait_vm_all();
+        __syncthreads();
+        for (int kt = 0; kt < nk; kt += 2) {
+            if (kt + 1 < nk) {
+                load_tile_lds<BM, NW>(A, lda, m0, M, k_begin + (kt + 1) * 64, sA1, wave, lane);
+                load_tile_lds<BN, NW>(B, ldb, n0, N, k_begin + (kt + 1) * 64, sB1, wave, lane);
+            }
+            compute(sA0, sB0);
+            wait_vm_all();
+            __syncthreads();
+            if (kt + 1 < nk) {
+                if (kt + 2 < nk) {
+                    load_tile_lds<BM, NW>(A, lda, m0, M, k_begin + (kt + 2) * 64, sA0, wave, lane);
+                    load_tile_lds<BN, NW>(B, ldb, n0, N, k_begin + (kt + 2) * 64, sB0, wave, lane);
+                }
+                compute(sA1, sB1);
+                wait_vm_all();
+                __syncthreads();
+            }
+        }
+    }
+
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+        const int m = m0 + wm * WTM + i * 16 + r;
+        if (m >= M) continue;
+        if constexpr (SPLIT) {
+#pragma unroll
+            for (int j = 0; j < TN; ++j) {
+                const int n = n0 + wn * WTN + j * 16 + 4 * g;
+                if (n < N)
+                    st4<float>(ws + ((size_t)blockIdx.y * M + m) * N + n, acc[i][j][0], acc[i][j][1],
+                               acc[i][j][2], acc[i][j][3]);
+            }
+        } else if constexpr (PAIRED) {
+#pragma unroll
+            for (int j = 0; j < TN; j += 2) {
+                const int n = n0 + wn * WTN + j * 16 + 4 * g;
+                if (n < N) {
+                    float gv[4] = {acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]};
+                    float uv[4] = {acc[i][j + 1][0], acc[i][j + 1][1], acc[i][j + 1][2], acc[i][j + 1][3]};
+                    epi.pair(m, n, gv, uv);
+                }
+            }
+        } else {
+#pragma unroll
+            for (int j = 0; j < TN; ++j) {
+                const int n = n0 + wn * WTN + j * 16 + 4 * g;
+                if (n < N) epi(m, n, acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]);
+            }
+        }
+    }
+}
+
 // ------------------------------------------------------------ fp32 GEMM --
 // 64 x 64 tile, BK 16, 256 threads; thread (ty, tx) owns rows 2ty, 2ty+1 and
 // columns grp*32 + q*4 + {0..3} and the same +16 (tx = grp*4 + q), so that a
@@ -325,10 +479,20 @@ __global__ void splitk_reduce_kernel(const float* __restrict__ ws, int splits, i
 // ------------------------------------------------------------- dispatch --
 
 // Tile and split choice depend only on (M, N, K).
-struct GemmPlan { int bm; int splits; int k_per_split; };
+struct GemmPlan { int bm; int bn; int splits; int k_per_split; bool big; };
 
 static GemmPlan plan_gemm(bool bf16, int M, int N, int K, size_t ws_floats) {
     GemmPlan p;
+    p.big = false;
+    p.bn = 0;
+    if (bf16 && M >= 256 && K % 64 == 0) {
+        p.big = true;
+        p.bm = 256;
+        p.bn = 256;
+        p.splits = 1;
+        p.k_per_split = K;
+        return p;
+    }
     if (!bf16) p.bm = 64;
     else if (M <= 16) p.bm = 16;
     else if (M <= 32) p.bm = 32;
@@ -354,6 +518,12 @@ static GemmPlan plan_gemm(bool bf16, int M, int N, int K, size_t ws_floats) {
 template <bool PAIRED, class Epi>
 static void launch_bf16(const GemmArgs& a, const GemmPlan& p, Epi epi, hipStream_t s) {
     const bool split = p.splits > 1;
+    if (p.big) {
+        dim3 grid(((a.M + 255) / 256) * ((a.N + 255) / 256), 1);
+        hipLaunchKernelGGL((gemm_bf16_big_kernel<256, 2, 4, PAIRED, false, Epi>), grid, dim3(512), 0, s,
+                           (const bf16_t*)a.A, a.lda, (const bf16_t*)a.B, a.ldb, a.M, a.N, a.K, a.K, a.ws, epi);
+        return;
+    }
     auto go = [&](auto kern, int bm, int bn) {
         dim3 grid(((a.M + bm - 1) / bm) * ((a.N + bn - 1) / bn), p.splits);
         hipLaunchKernelGGL(kern, grid, dim3(256), 0, s, (const bf16_t*)a.A, a.lda,
