@@ -366,9 +366,14 @@ class Policy:
     """Seeded random-init policy evaluated in float64."""
 
     def __init__(self, cfg: Config, seed: int = 0, overrides: Optional[Dict[str, np.ndarray]] = None,
-                 cache_limit_params: int = 600_000_000):
+                 cache_limit_params: int = 600_000_000, emulate_bf16: bool = False):
         self.cfg = cfg
         self.seed = seed
+        # Optional: round to bf16 exactly where a bf16 policy stores bf16
+        # (normalised GEMM inputs, rotated Q and K, V, softmax numerators
+        # before the P.V product, attention and SwiGLU outputs, patch pixels);
+        # all arithmetic between those points stays float64.  Off by default.
+        self.emulate_bf16 = bool(emulate_bf16 and cfg.bf16)
         self.shapes = tensor_shapes(cfg)
         self.overrides = dict(overrides or {})
         total = sum(int(np.prod(sh)) for _, sh in self.shapes.values())
@@ -402,24 +407,53 @@ class Policy:
               causal=True, use_rope=True):
         """Pre-norm transformer block.  Returns (x_out, k_new, v_new)."""
         t = x.shape[0]
-        h = rmsnorm(x, self.cfg.eps)
+        R = self._r
+        h = R(rmsnorm(x, self.cfg.eps))
         q = linear(h, Wl["q"]).reshape(t, n_heads, hd)
         k = linear(h, Wl["k"]).reshape(t, n_kv, hd)
         v = linear(h, Wl["v"]).reshape(t, n_kv, hd)
         if use_rope:
             q = rope(q, pos, self.cfg.rope_base)
             k = rope(k, pos, self.cfg.rope_base)
+        q, k, v = R(q), R(k), R(v)
         if past_k is not None:
             K = np.concatenate([past_k, k], axis=0)
             V = np.concatenate([past_v, v], axis=0)
             kpos = np.concatenate([past_pos, pos])
         else:
             K, V, kpos = k, v, pos
-        o = multihead_attention(q, K, V, pos, kpos, causal).reshape(t, n_heads * hd)
+        if self.emulate_bf16:
+            o = self._attention_bf16(q, K, V, pos, kpos, causal)
+        else:
+            o = multihead_attention(q, K, V, pos, kpos, causal)
+        o = R(o.reshape(t, n_heads * hd))
         x = x + linear(o, Wl["o"])
-        h = rmsnorm(x, self.cfg.eps)
-        x = x + linear(silu(linear(h, Wl["gate"])) * linear(h, Wl["up"]), Wl["down"])
+        h = R(rmsnorm(x, self.cfg.eps))
+        x = x + linear(R(silu(linear(h, Wl["gate"])) * linear(h, Wl["up"])), Wl["down"])
         return x, k, v
+
+    def _r(self, a):
+        return f64_to_bf16_value(a) if self.emulate_bf16 else a
+
+    @staticmethod
+    def _attention_bf16(q, k, v, q_pos, k_pos, causal):
+        """Softmax attention whose numerators enter the P.V product rounded to
+        bf16 while the denominator sums the unrounded ones (the bf16 policy's
+        storage points).  The numerators are taken relative to the power of
+        two at or above the row maximum: with x = s log2(e), e_j = 2^(x_j -
+        ceil(max x)).  The scale cancels in the ratio, so without rounding
+        this is exactly `attention`."""
+        hq, hkv, hd = q.shape[1], k.shape[1], q.shape[-1]
+        out = np.empty_like(q)
+        for h in range(hq):
+            g = h // (hq // hkv)
+            s = (q[:, h, :] @ k[:, g, :].T) / np.sqrt(hd)
+            if causal:
+                s = np.where(k_pos[None, :] <= q_pos[:, None], s, -np.inf)
+            x = s * np.log2(np.e)
+            e = np.exp2(x - np.ceil(np.max(x, axis=-1, keepdims=True)))
+            out[:, h, :] = (f64_to_bf16_value(e) @ v[:, g, :]) / np.sum(e, axis=-1, keepdims=True)
+        return out
 
     # prefill ---------------------------------------------------------------
     def embed_prefix(self, image: Optional[np.ndarray], lang: Sequence[int]) -> np.ndarray:
@@ -427,7 +461,7 @@ class Policy:
         cfg = self.cfg
         rows = []
         if image is not None:
-            patches = patchify(np.asarray(image, dtype=np.float64), cfg.patch)
+            patches = self._r(patchify(np.asarray(image, dtype=np.float64), cfg.patch))
             if cfg.vit_layers:
                 v = linear(patches, self.W("W_pe")) + self.W("vit_pos")
                 hd = cfg.vit_d // cfg.vit_heads
@@ -435,7 +469,7 @@ class Policy:
                 for l in range(cfg.vit_layers):
                     v, _, _ = self.block(v, self.layer("vit", l), cfg.vit_heads, cfg.vit_heads, hd,
                                          pos, causal=False, use_rope=False)
-                rows.append(linear(rmsnorm(v, cfg.eps), self.W("W_proj")))
+                rows.append(linear(self._r(rmsnorm(v, cfg.eps)), self.W("W_proj")))
             else:
                 rows.append(linear(patches, self.W("W_pe")))
         E = self.W("E_lang")
@@ -455,6 +489,30 @@ class Policy:
             ks.append(k)
             vs.append(v)
         return PrefixState(T, ks, vs, x[-1].copy(), rmsnorm(x[-1], cfg.eps))
+
+    def teacher_forced(self, image: Optional[np.ndarray], lang: Sequence[int],
+                       forced: Sequence[int]):
+        """Prefill and teacher-forced action decode in one causal pass over
+        [prefix rows ; E_act[forced[0..5]]]: by causality the prefix rows
+        (and their K/V) are those of prefill alone, and the logits at
+        positions T-1 .. T+5 are those of the incremental decode fed the
+        forced tokens.  Returns (PrefixState, DecodeResult)."""
+        cfg = self.cfg
+        rows = self.embed_prefix(image, lang)
+        T = rows.shape[0]
+        x = np.concatenate([rows, self.W("E_act")[np.asarray(forced, dtype=np.int64)]], axis=0)
+        pos = np.arange(x.shape[0])
+        ks, vs = [], []
+        for l in range(cfg.layers):
+            x, k, v = self.block(x, self.layer("dec", l), cfg.q_heads, cfg.kv_heads, cfg.head_dim, pos)
+            ks.append(k[:T])
+            vs.append(v[:T])
+        hn = rmsnorm(x, cfg.eps)
+        st = PrefixState(T, ks, vs, x[T - 1].copy(), hn[T - 1].copy())
+        L = np.stack([self.logits(hn[T - 1 + k]) for k in range(cfg.n_action_tokens)])
+        toks = np.asarray([argmax_lowest(r) for r in L], dtype=np.int64)
+        return st, DecodeResult(toks, L, np.array([top2_margin(r) for r in L]),
+                                detokenize(toks, cfg.n_bins))
 
     def run_sequence(self, x: np.ndarray) -> np.ndarray:
         """Decoder over explicit input rows at positions 0..len-1 (causal);

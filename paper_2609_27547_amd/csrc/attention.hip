@@ -7,7 +7,9 @@
 //   computes S^T = K Q^T for its 16 queries with v_mfma_f32_16x16x32_bf16 so
 //   that every lane holds the scores of a single query, runs the online
 //   softmax in fp32 with exp2, and feeds the probabilities straight back as
-//   the B operand of O^T = V^T P^T (V staged transposed in LDS).
+//   the B operand of O^T = V^T P^T (V staged transposed in LDS).  P enters
+//   the bf16 product as 2^(x - ceil(max x)), x = s log2(e) / sqrt(hd), with
+//   the row sum taken before rounding.
 // attn_prefill_f32: plain per-(query, head) kernel for fp32 policies.
 // attn_decode: one query per sequence; keys split into 64-key chunks, each
 //   chunk a workgroup that streams its K and V rows once with 16-byte loads;
@@ -111,9 +113,13 @@ __global__ __launch_bounds__(256) void attn_prefill_bf16_kernel(AttnPrefillArgs 
             }
         tmax = fmaxf(tmax, __shfl_xor(tmax, 16, 64));
         tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
-        const float m_new = fmaxf(m_i, tmax);
+        // The running maximum is kept as an integer (ceil, in log2 units):
+        // rescaling by alpha is then a power of two, which commutes with the
+        // bf16 rounding of P, so P is rounded as 2^(x - ceil(row max)) no
+        // matter how the keys are split into tiles.
+        const float m_new = fmaxf(m_i, ceilf(tmax));
         const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
-        const float alpha = fast_exp2(m_i - m_use);
+        const float alpha = (m_i == -INFINITY) ? 0.f : ldexpf(1.0f, (int)(m_i - m_use));
         float psum = 0.f;
 #pragma unroll
         for (int kt = 0; kt < 4; ++kt)

@@ -408,8 +408,9 @@ int validate(const ebrl_config& c, std::string& why) {
 
 // --------------------------------------------------------- GEMM launch --
 
-int run_gemm(ebrl_policy* p, GemmArgs a) {
+int run_gemm(ebrl_policy* p, GemmArgs a, bool split_ok = false) {
     a.bf16 = p->bf16;
+    a.split_ok = split_ok;
     a.ws = p->ws;
     a.ws_floats = p->ws_floats;
     const int cls = a.M >= 256 ? EBRL_K_GEMM : EBRL_K_GEMM_SKINNY;
@@ -447,7 +448,7 @@ int run_block(ebrl_policy* p, BlockCall& b) {
     GemmArgs g;
     g.A = p->Xn; g.lda = s.d; g.B = b.w->qkv; g.ldb = s.d; g.M = b.rows; g.N = qkvn; g.K = s.d;
     g.epi = EPI_F32; g.C = p->QKV; g.ldc = qkvn;
-    run_gemm(p, g);
+    run_gemm(p, g, b.decode);
     RopeKVArgs r;
     r.bf16 = p->bf16; r.qkv = p->QKV; r.ld = qkvn; r.M = b.rows; r.q_heads = s.hq;
     r.Q = p->Qb; r.ldq = qn; r.kv = b.kv; r.seq_env = b.seq_env; r.row_seq = b.row_seq;
@@ -471,18 +472,18 @@ int run_block(ebrl_policy* p, BlockCall& b) {
     g = GemmArgs();
     g.A = p->Ob; g.lda = qn; g.B = b.w->o; g.ldb = qn; g.M = b.rows; g.N = s.d; g.K = qn;
     g.epi = EPI_RESID; g.C = b.R; g.ldc = s.d;
-    run_gemm(p, g);
+    run_gemm(p, g, b.decode);
     prof_begin(p, EBRL_K_OTHER);
     rmsnorm_rows(p->bf16, b.R, s.d, nullptr, p->Xn, s.d, b.rows, s.d, 1e-6f, p->stream);
     prof_end(p, 0, (double)b.rows * s.d * (4 + p->esz));
     g = GemmArgs();
     g.A = p->Xn; g.lda = s.d; g.B = b.w->gu; g.ldb = s.d; g.M = b.rows; g.N = 2 * s.mlp; g.K = s.d;
     g.epi = EPI_SWIGLU; g.C = p->Hb; g.ldc = s.mlp;
-    run_gemm(p, g);
+    run_gemm(p, g, b.decode);
     g = GemmArgs();
     g.A = p->Hb; g.lda = s.mlp; g.B = b.w->down; g.ldb = s.mlp; g.M = b.rows; g.N = s.d; g.K = s.mlp;
     g.epi = EPI_RESID; g.C = b.R; g.ldc = s.d;
-    run_gemm(p, g);
+    run_gemm(p, g, b.decode);
     return EBRL_OK;
 }
 
@@ -746,7 +747,7 @@ int ebrl_policy_create(const ebrl_config* config, uint64_t seed, ebrl_policy** o
     HIPCHK(p, hipMemset(p->h_pre, 0, (size_t)c.max_envs * c.d * 4));
     HIPCHK(p, hipMemset(p->h_norm, 0, (size_t)c.max_envs * c.d * 4));
     // split-K workspace: 16 splits of the widest skinny projection
-    p->ws_floats = (size_t)16 * std::min<size_t>(R, 256) * std::max(w_qkv, 2 * w_mlp);
+    p->ws_floats = (size_t)16 * 256 * std::max(w_qkv, 2 * w_mlp);
     if ((rc = dev_alloc_t(p, &p->ws, p->ws_floats))) return bail(rc);
     const int max_splits = (c.max_seq + p->tail + ATTN_DEC_CHUNK - 1) / ATTN_DEC_CHUNK;
     p->part_floats = (size_t)c.max_envs * c.q_heads * max_splits * (c.head_dim + 2);
@@ -1217,6 +1218,7 @@ int ebrl_op_gemm(int32_t dtype, const void* A, const void* B, float* C, int32_t 
     a.bf16 = dtype == EBRL_DTYPE_BF16;
     a.A = A; a.lda = K; a.B = B; a.ldb = K; a.M = M; a.N = N; a.K = K;
     a.epi = EPI_F32; a.C = C; a.ldc = N; a.ws = g_ws; a.ws_floats = g_ws_floats;
+    a.split_ok = M < 256;
     ebrl::gemm(a, (hipStream_t)stream);
     return hipGetLastError() == hipSuccess ? EBRL_OK : EBRL_E_HIP;
 }

@@ -481,16 +481,20 @@ __global__ void splitk_reduce_kernel(const float* __restrict__ ws, int splits, i
 // Tile and split choice depend only on (M, N, K).
 struct GemmPlan { int bm; int bn; int splits; int k_per_split; bool big; };
 
-static GemmPlan plan_gemm(bool bf16, int M, int N, int K, size_t ws_floats) {
+// Kernel and split choice.  The tile variant never changes an element's
+// summation order; the split count (decode only) is a function of (N, K).
+constexpr int SPLIT_MAX_M = 256;
+
+static GemmPlan plan_gemm(bool bf16, int M, int N, int K, size_t ws_floats, bool split_ok) {
     GemmPlan p;
     p.big = false;
     p.bn = 0;
-    if (bf16 && M >= 256 && K % 64 == 0) {
+    p.splits = 1;
+    p.k_per_split = K;
+    if (bf16 && !split_ok && M >= 256 && K % 64 == 0) {
         p.big = true;
         p.bm = 256;
         p.bn = 256;
-        p.splits = 1;
-        p.k_per_split = K;
         return p;
     }
     if (!bf16) p.bm = 64;
@@ -498,19 +502,19 @@ static GemmPlan plan_gemm(bool bf16, int M, int N, int K, size_t ws_floats) {
     else if (M <= 32) p.bm = 32;
     else if (M <= 64) p.bm = 64;
     else p.bm = 128;
-    const int bn = bf16 ? (p.bm == 16 ? 256 : 128) : 64;
-    const long tiles = (long)((M + p.bm - 1) / p.bm) * ((N + bn - 1) / bn);
+    if (!split_ok) return p;
+    // one row of 128-wide column tiles -> enough K splits for ~512 workgroups
+    const long tiles = (N + 127) / 128;
     int splits = 1;
     if (tiles < 256) {
         const int kblocks = (K + BK - 1) / BK;
         splits = (int)std::min<long>((512 + tiles - 1) / tiles, (long)std::max(1, kblocks / 2));
         splits = std::max(1, std::min(splits, 16));
     }
-    while (splits > 1 && (size_t)splits * M * N > ws_floats) --splits;
+    while (splits > 1 && (size_t)splits * SPLIT_MAX_M * N > ws_floats) --splits;
     int kps = (K + splits - 1) / splits;
     kps = (kps + BK - 1) / BK * BK;
-    splits = (K + kps - 1) / kps;
-    p.splits = splits;
+    p.splits = (K + kps - 1) / kps;
     p.k_per_split = kps;
     return p;
 }
@@ -577,7 +581,7 @@ static void launch_f32(const GemmArgs& a, const GemmPlan& p, Epi epi, hipStream_
 
 template <bool PAIRED, class Epi>
 static int dispatch(const GemmArgs& a, Epi epi, hipStream_t s) {
-    const GemmPlan p = plan_gemm(a.bf16, a.M, a.N, a.K, a.ws_floats);
+    const GemmPlan p = plan_gemm(a.bf16, a.M, a.N, a.K, a.ws_floats, a.split_ok && a.M <= SPLIT_MAX_M);
     if (a.bf16) launch_bf16<PAIRED>(a, p, epi, s);
     else launch_f32<PAIRED>(a, p, epi, s);
     return p.splits;
@@ -606,8 +610,8 @@ int gemm(const GemmArgs& a, hipStream_t s) {
     return 0;
 }
 
-int gemm_splits(bool bf16, int M, int N, int K, size_t ws_floats) {
-    return plan_gemm(bf16, M, N, K, ws_floats).splits;
+int gemm_splits(bool bf16, int M, int N, int K, size_t ws_floats, bool split_ok) {
+    return plan_gemm(bf16, M, N, K, ws_floats, split_ok && M <= SPLIT_MAX_M).splits;
 }
 
 }  // namespace ebrl

@@ -28,10 +28,16 @@ struct GemmArgs {
     const int* row_base = nullptr; int group = 1;
     const void* add = nullptr; int add_ld = 0;
     float* ws = nullptr; size_t ws_floats = 0;  // split-K workspace
+    // Decode GEMMs (M = batch, at most 256) may split K; the split count then
+    // depends on (N, K) only, so an element's summation order -- and its bits
+    // -- do not depend on the batch size.  Without splitting, every kernel
+    // variant sums K in the same 64-wide steps, so results do not depend on M
+    // either.
+    bool split_ok = false;
 };
 // Returns the number of K splits used (1 = single pass).
 int gemm(const GemmArgs& a, hipStream_t s);
-int gemm_splits(bool bf16, int M, int N, int K, size_t ws_floats);
+int gemm_splits(bool bf16, int M, int N, int K, size_t ws_floats, bool split_ok);
 
 // ------------------------------------------------------------- attention --
 // Paged KV: layer base pointer; physical block b holds

@@ -1,0 +1,190 @@
+"""Parity at the workloads' full sizes, in the launch configuration the
+benchmark times, on outputs the oracle can compute env by env (envs are
+independent, so a sampled env checks the whole batch's code path).
+
+* 7B-class VLA (ViT + 32-layer decoder), 32 envs: sampled env against the
+  oracle's teacher-forced single pass.
+* flow-matching expert on the GQA backbone, 64 envs: sampled env's velocity
+  at tau = 1 and its denoised chunk.
+* ragged asynchronous decode on the 7B-class model: a 128-slot pool of
+  language-only prefixes (lengths U[200, 320]); calls of random size on the
+  whole GPU and on a CU-masked stream give bitwise identical outputs, and a
+  sampled env matches the oracle.
+
+Reference: the exact oracle (float64 throughout).  Bound: 2e-2, except where
+rounding to bf16 at the bf16 policy's storage points (GEMM inputs, Q/K/V, P,
+attention and SwiGLU outputs) already moves the exact result further on the
+same input -- measured with the oracle's bf16-emulating mode -- where the
+bound is 1.5 times that deviation.  That happens for the 32-layer decoder on
+a language-only prefix: bf16 rounding flips cascade layer by layer, so any
+bf16-operand implementation lands about that far from the exact result (two
+bf16 implementations differ from each other by a similar amount).  The token
+margin threshold is scaled from the same measurement.
+"""
+import numpy as np
+import pytest
+
+import synth_inputs
+from oracle import model as M
+from tests import parity as P
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+from paper_2609_27547_amd import ebrl as E  # noqa: E402
+
+
+def _dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def report(name, value):
+    print(f"PARITY {name} {value:.3e}", flush=True)
+
+
+@pytest.fixture(scope="module")
+def oracle_7b():
+    exact = M.Policy(M.PRESETS[3], seed=0)
+    emu = M.Policy(M.PRESETS[3], seed=0, emulate_bf16=True)
+    emu._raw = exact._raw           # same generated weights, generated once
+    return exact, emu
+
+
+def _bound(y_emu, y_exact):
+    return max(P.TOL_BF16, 1.5 * P.row_rel_err(y_emu, y_exact))
+
+
+def _check_prefix(pol, e, st, st_emu, layers, tag):
+    """Returns the hidden-state bound used for this input."""
+    report(f"{tag}.oracle_emulated_vs_exact", P.row_rel_err(st_emu.h_last_pre, st.h_last_pre))
+    bound = _bound(st_emu.h_last_pre, st.h_last_pre)
+    h = pol.read_state(E.STATE_H_LAST_PRE, e)
+    err = P.row_rel_err(h, st.h_last_pre)
+    report(f"{tag}.h_last_pre", err)
+    report(f"{tag}.h_last_pre_vs_emulated", P.row_rel_err(h, st_emu.h_last_pre))
+    assert err < bound
+    hn = pol.read_state(E.STATE_H_LAST, e)
+    assert P.row_rel_err(hn, st.h_last) < _bound(st_emu.h_last, st.h_last)
+    for l in layers:
+        for what, ref, emu in [(E.STATE_K, st.k[l], st_emu.k[l]), (E.STATE_V, st.v[l], st_emu.v[l])]:
+            g = P.bf16_to_f64(pol.read_state(what, e, l)).reshape(st.T, -1)
+            ref, emu = ref.reshape(st.T, -1), emu.reshape(st.T, -1)
+            err = P.row_rel_err(g, ref)
+            report(f"{tag}.{'k' if what == E.STATE_K else 'v'}{l}", err)
+            assert err < _bound(emu, ref)
+    return bound
+
+
+def _check_tokens(tok, r, r_emu, tag):
+    """Margin rule against the exact oracle; the threshold is 1e-2 or twice
+    the logit deviation that bf16 storage alone causes on this input."""
+    dev = float(np.max(np.abs(r_emu.logits - r.logits)))
+    thr = max(P.MARGIN, 2 * dev)
+    report(f"{tag}.oracle_emulated_logit_dev", dev)
+    close = 0
+    for k, t in enumerate(tok):
+        if r.margins[k] > thr:
+            assert int(t) == int(r.tokens[k]), (k, int(t), int(r.tokens[k]), r.margins[k])
+        else:
+            close += 1
+            assert r.logits[k][int(t)] >= r.logits[k].max() - thr
+    report(f"{tag}.tokens_decided_within_threshold", close)
+
+
+def test_7b_vla_full_batch_sampled_env(oracle_7b):
+    cfg = M.PRESETS[3]
+    ids = list(range(32))
+    img = synth_inputs.pixels(1003, ids, cfg.n_cams, cfg.img, cfg.img)
+    lang = synth_inputs.lang_ids(1003, ids, cfg.n_lang, cfg.vocab)
+    pol = E.Policy(3, seed=0)
+    pol.prefill(ids, images=_dev(img), lang_ids=_dev(lang))
+    tok, act, mar = pol.decode_actions(ids)
+    torch.cuda.synchronize()
+    tok = tok.cpu().numpy()
+    e = 19
+    exact, emu = oracle_7b
+    st, r = exact.teacher_forced(img[e], lang[e], tok[e, :-1])
+    st2, r2 = emu.teacher_forced(img[e], lang[e], tok[e, :-1])
+    bound = _check_prefix(pol, e, st, st2, [0, 31], "7b")
+    assert bound == P.TOL_BF16          # image prefix: the plain 2e-2 holds
+    _check_tokens(tok[e], r, r2, "7b")
+    pol.close()
+
+
+def test_flow_expert_full_batch_sampled_env():
+    cfg = M.PRESETS[4]
+    ids = list(range(64))
+    img = synth_inputs.pixels(1004, ids, cfg.n_cams, cfg.img, cfg.img)
+    lang = synth_inputs.lang_ids(1004, ids, cfg.n_lang, cfg.vocab)
+    noise = synth_inputs.flow_noise(4, ids, cfg.chunk, cfg.adim)
+    pol = E.Policy(4, seed=0)
+    pol.prefill(ids, images=_dev(img), lang_ids=_dev(lang))
+    out = pol.flow_denoise(ids, _dev(noise))
+    torch.cuda.synchronize()
+    out = out.cpu().numpy()
+    ref = M.Policy(cfg, seed=0)
+    emu = M.Policy(cfg, seed=0, emulate_bf16=True)
+    emu._raw = ref._raw
+    e = 11
+    st, st2 = ref.prefill(img[e], lang[e]), emu.prefill(img[e], lang[e])
+    assert _check_prefix(pol, e, st, st2, [0, 17], "flow") == P.TOL_BF16
+    x, v0 = ref.flow_denoise(st, noise[e], return_v0=True)
+    x2, v02 = emu.flow_denoise(st2, noise[e], return_v0=True)
+    gv0 = pol.read_state(E.STATE_FLOW_V0, e)
+    ev, ex = P.row_rel_err(gv0, v0), P.row_rel_err(out[e], x)
+    report("flow.v0", ev)
+    report("flow.x10", ex)
+    report("flow.v0_vs_emulated", P.row_rel_err(gv0, v02))
+    assert ev < P.TOL_BF16 and ex < P.TOL_BF16
+    pol.close()
+
+
+def balanced_mask(frac_quarters: int, n_cu: int = 256):
+    """CU mask words selecting frac_quarters/4 of the CUs, 8-CU runs spread so
+    that every XCD gets the same share whether the runtime numbers CUs XCD by
+    XCD or round-robin across XCDs."""
+    words = [0] * (n_cu // 32)
+    for i in range(n_cu):
+        if (i // 8) % 4 < frac_quarters:
+            words[i // 32] |= 1 << (i % 32)
+    return words
+
+
+def test_ragged_decode_partitions_bitwise_and_sampled_parity(oracle_7b):
+    cfg = M.PRESETS[3]
+    pool = 128
+    T = synth_inputs.ragged_prefix_lengths(5, pool, 200, 320)
+    lang = synth_inputs.lang_ids(1005, list(range(pool)), 320, cfg.vocab)
+    pol = E.Policy(3, seed=0, max_envs=pool, max_seq=320)
+    pol.prefill(list(range(pool)), images=None, lang_ids=_dev(lang), lang_len=T)
+    calls = synth_inputs.ragged_calls(5, 3, pool, 128)
+    full = []
+    for ids in calls:
+        tok, _, mar = pol.decode_actions(ids)
+        full.append((tok.clone(), mar.clone()))
+    torch.cuda.synchronize()
+    s25 = E.create_cu_masked_stream(0, balanced_mask(1))
+    try:
+        pol.bind_stream(s25)
+        for ids, (tok_f, mar_f) in zip(calls, full):
+            tok, _, mar = pol.decode_actions(ids)
+            torch.cuda.synchronize()
+            assert torch.equal(tok, tok_f) and torch.equal(mar, mar_f)
+        pol.bind_stream(torch.cuda.current_stream().cuda_stream)
+    finally:
+        torch.cuda.synchronize()
+        E.destroy_stream(s25)
+    # the same env decoded in another batch composition: bitwise equal
+    ids0 = calls[0]
+    e = int(ids0[len(ids0) // 2])
+    tok_solo, _, mar_solo = pol.decode_actions([e])
+    torch.cuda.synchronize()
+    j = list(ids0).index(e)
+    assert torch.equal(tok_solo[0], full[0][0][j]) and torch.equal(mar_solo[0], full[0][1][j])
+    tok_e = full[0][0][j].cpu().numpy()
+    exact, emu = oracle_7b
+    st, r = exact.teacher_forced(None, lang[e][:T[e]], tok_e[:-1])
+    st2, r2 = emu.teacher_forced(None, lang[e][:T[e]], tok_e[:-1])
+    _check_prefix(pol, e, st, st2, [0, 31], "ragged")
+    _check_tokens(tok_e, r, r2, "ragged")
+    pol.close()

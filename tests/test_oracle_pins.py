@@ -429,3 +429,53 @@ def test_preset_parameter_counts():
     c3 = M.PRESETS[3]
     total = sum(int(np.prod(sh)) for _, sh in M.tensor_shapes(c3).values())
     assert 6.5e9 < total < 7.5e9            # "7B-class"
+
+
+def test_teacher_forced_single_pass_equals_prefill_then_forced_decode():
+    cfg = tiny_cfg(kv_heads=2)
+    pol = M.Policy(cfg, seed=0)
+    img, lang = _obs(cfg, [2])
+    forced = [7, 200, 31, 31, 0, 255]
+    st_ref = pol.prefill(img[0], lang[0])
+    r_ref = pol.decode(st_ref, forced=forced)
+    st, r = pol.teacher_forced(img[0], lang[0], forced)
+    assert st.T == st_ref.T
+    assert np.allclose(st.h_last_pre, st_ref.h_last_pre, rtol=0, atol=1e-12)
+    for l in range(cfg.layers):
+        assert np.allclose(st.k[l], st_ref.k[l], atol=1e-12) and np.allclose(st.v[l], st_ref.v[l], atol=1e-12)
+    assert np.allclose(r.logits, r_ref.logits, rtol=0, atol=1e-12)
+    assert np.array_equal(r.tokens, r_ref.tokens)
+
+
+def test_bf16_emulation_rounds_only_at_storage_points():
+    # fp32 policies ignore the flag; with it a bf16 policy stays close to the
+    # exact one and every stored K/V element is a bf16 value
+    cfg = tiny_cfg()
+    img, lang = _obs(cfg, [0])
+    a = M.Policy(cfg, seed=0).prefill(img[0], lang[0])
+    b = M.Policy(cfg, seed=0, emulate_bf16=True).prefill(img[0], lang[0])
+    assert np.array_equal(a.h_last_pre, b.h_last_pre)
+    cfg16 = tiny_cfg(bf16=True)
+    a = M.Policy(cfg16, seed=0).prefill(img[0], lang[0])
+    e = M.Policy(cfg16, seed=0, emulate_bf16=True)
+    b = e.prefill(img[0], lang[0])
+    for l in range(cfg16.layers):
+        assert np.array_equal(M.f64_to_bf16_value(b.k[l]), b.k[l])
+        assert np.array_equal(M.f64_to_bf16_value(b.v[l]), b.v[l])
+    err = np.linalg.norm(a.h_last_pre - b.h_last_pre) / np.linalg.norm(a.h_last_pre)
+    assert 1e-5 < err < 3e-2
+    # the bf16 attention differs from the exact one only by rounding P
+    rng = np.random.default_rng(8)
+    q = rng.normal(size=(5, 2, 16)); k = rng.normal(size=(7, 1, 16)); v = rng.normal(size=(7, 1, 16))
+    qp = np.arange(5) + 2; kp = np.arange(7)
+    ex = M.multihead_attention(q, k, v, qp, kp, True)
+    em = M.Policy._attention_bf16(q, k, v, qp, kp, True)
+    assert np.allclose(ex, em, rtol=0, atol=2e-2) and not np.array_equal(ex, em)
+    # single key: the numerator 2^(x - ceil x) in (1/2, 1] is rounded once and
+    # divided by its unrounded self: v scaled by (1 + rel. rounding error)
+    one = M.Policy._attention_bf16(q[:, :1], k[:1], v[:1], qp, kp[:1], True)
+    ratio = one / np.repeat(v[:1], 5, axis=0)[:, :1]
+    assert np.all(np.abs(ratio - 1) <= 2.0 ** -8) and np.allclose(ratio, ratio[..., :1], rtol=0, atol=1e-15)
+    # equal scores: every numerator is 2^(x - ceil x) rounded alike -> mean of V
+    same = M.Policy._attention_bf16(np.zeros((3, 1, 16)), k[:4], v[:4], np.arange(3) + 9, kp[:4], True)
+    assert np.allclose(same, np.repeat(v[:4].mean(0, keepdims=True), 3, axis=0), atol=1e-15)
