@@ -32,6 +32,8 @@ WORKLOADS = {
     "tiny-fp32": (1, 8, 1001),
     "small-bf16": (2, 64, 1002),
     "7b-bf16": (3, 32, 1003),
+    "flow-bf16": (4, 64, 1004),
+    "ragged-7b": (3, 128, 1005),
 }
 PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA
 PEAK_FP32_TFLOPS = 157.3      # MI355X fp32 vector
@@ -42,8 +44,9 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def cpu_baseline(preset: int, obs_seed: int, n_sample: int):
-    """The oracle as it stands, on this host's cores, on n_sample envs."""
+def cpu_baseline(workload: str, n_sample: int):
+    """The oracle as it stands, on this host's cores, on n_sample envs of the
+    same workload (envs are independent, so the rate scales per env)."""
     import synth_inputs
     from oracle import model as M
     try:
@@ -51,6 +54,7 @@ def cpu_baseline(preset: int, obs_seed: int, n_sample: int):
         cores = max([d.get("num_threads", 1) for d in threadpool_info()] + [1])
     except Exception:
         cores = os.cpu_count()
+    preset, _, obs_seed = WORKLOADS[workload]
     cfg = M.PRESETS[preset]
     ids = list(range(n_sample))
     img = synth_inputs.pixels(obs_seed, ids, cfg.n_cams, cfg.img, cfg.img)
@@ -61,13 +65,92 @@ def cpu_baseline(preset: int, obs_seed: int, n_sample: int):
         pol.W(name)
     t_w = time.perf_counter() - t
     t = time.perf_counter()
+    per_env = cfg.chunk if cfg.exp_layers else 1
     for i in ids:
-        pol.decode(pol.prefill(img[i], lang[i]))
+        st = pol.prefill(img[i], lang[i])
+        if cfg.exp_layers:
+            pol.flow_denoise(st, synth_inputs.flow_noise(4, [i], cfg.chunk, cfg.adim)[0])
+        else:
+            pol.decode(st)
     dt = time.perf_counter() - t
-    return {"value": round(n_sample / dt, 4), "unit": "actions/s", "cores": int(cores), "kind": "oracle",
-            "sample": f"{n_sample} env(s) of the same workload: prefill + 6 decode steps in float64 "
-                      f"(numpy/BLAS), {dt:.1f} s; weight generation ({t_w:.1f} s) excluded",
+    what = "prefill + 10 Euler steps of the expert" if cfg.exp_layers else "prefill + 6 decode steps"
+    return {"value": round(n_sample * per_env / dt, 4), "unit": "actions/s", "cores": int(cores), "kind": "oracle",
+            "sample": f"{n_sample} env(s) of the same workload: {what} in float64 (numpy/BLAS), {dt:.1f} s; "
+                      f"weight generation ({t_w:.1f} s) excluded",
             "seconds": round(dt, 3)}
+
+
+def balanced_mask(quarters: int, n_cu: int = 256):
+    """CU mask words for quarters/4 of the CUs: runs of 8 CUs spread so every
+    XCD gets the same share whether CUs are numbered XCD by XCD or round-robin
+    across XCDs."""
+    words = [0] * (n_cu // 32)
+    for i in range(n_cu):
+        if (i // 8) % 4 < quarters:
+            words[i // 32] |= 1 << (i % 32)
+    return words
+
+
+class Workload:
+    """Sets up one workload's policy and resident inputs; step() enqueues
+    one pass of the hot path and returns the actions it produces."""
+
+    def __init__(self, name, E, torch, steps):
+        import synth_inputs
+        self.name = name
+        preset, n, seed = WORKLOADS[name]
+        self.torch = torch
+        kw = {}
+        if name == "ragged-7b":
+            kw = dict(max_envs=128, max_seq=320)
+        t = time.perf_counter()
+        self.pol = E.Policy(preset, seed=0, stream=torch.cuda.current_stream().cuda_stream, **kw)
+        log(f"policy {name} created in {time.perf_counter() - t:.1f} s")
+        c = self.pol.cfg
+        self.c = c
+        self.n = n
+        ids = list(range(n))
+        self.ids = ids
+        dev = lambda a: torch.from_numpy(a).cuda()
+        if name == "ragged-7b":
+            # env pool: language-only prefixes of length U[200, 320] (prefilled once)
+            self.T = synth_inputs.ragged_prefix_lengths(5, n, 200, 320)
+            lang = synth_inputs.lang_ids(seed, ids, 320, c.vocab)
+            self.pol.prefill(ids, images=None, lang_ids=dev(lang), lang_len=self.T)
+            self.calls = synth_inputs.ragged_calls(5, max(steps, 1), n, 128)
+            self.call_i = 0
+            self.tok = torch.empty((128, c.n_action_tokens), dtype=torch.int32, device="cuda")
+            self.act = torch.empty((128, c.n_action_tokens), dtype=torch.float32, device="cuda")
+            return
+        self.img = dev(synth_inputs.pixels(seed, ids, c.n_cams, c.img, c.img))
+        self.lang = dev(synth_inputs.lang_ids(seed, ids, c.n_lang, c.vocab))
+        if c.exp_layers:
+            self.noise = dev(synth_inputs.flow_noise(4, ids, c.chunk, c.adim))
+            self.out = torch.empty_like(self.noise)
+        else:
+            self.tok = torch.empty((n, c.n_action_tokens), dtype=torch.int32, device="cuda")
+            self.act = torch.empty((n, c.n_action_tokens), dtype=torch.float32, device="cuda")
+
+    def prefill(self):
+        self.pol.prefill(self.ids, images=self.img, lang_ids=self.lang)
+
+    def head(self):
+        if self.c.exp_layers:
+            self.pol.flow_denoise(self.ids, self.noise, out=self.out)
+            return self.n * self.c.chunk
+        self.pol.decode_actions(self.ids, tokens=self.tok, actions=self.act, margins=None, with_margin=False)
+        return self.n
+
+    def step(self):
+        if self.name == "ragged-7b":
+            ids = self.calls[self.call_i % len(self.calls)]
+            self.call_i += 1
+            k = len(ids)
+            self.pol.decode_actions(ids, tokens=self.tok[:k], actions=self.act[:k], margins=None,
+                                    with_margin=False)
+            return k
+        self.prefill()
+        return self.head()
 
 
 def main():
@@ -77,6 +160,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="small-bf16", choices=sorted(WORKLOADS))
     ap.add_argument("--cpu-sample", type=int, default=16, help="envs in the oracle sample (0 = skip)")
+    ap.add_argument("--partitions", action="store_true",
+                    help="also time the steps on CU-masked streams of 25/50/75%% of the CUs")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}); environments "
@@ -85,66 +170,62 @@ def main():
         sys.exit(2)
 
     import torch
-    import synth_inputs
     from paper_2609_27547_amd import ebrl as E
 
-    preset, n, obs_seed = WORKLOADS[args.workload]
     torch.cuda.set_device(0)
     stream = torch.cuda.current_stream()
-    t = time.perf_counter()
-    pol = E.Policy(preset, seed=0, stream=stream.cuda_stream)
-    log(f"policy {args.workload} created in {time.perf_counter() - t:.1f} s")
-    c = pol.cfg
-    ids = list(range(n))
-    img = synth_inputs.pixels(obs_seed, ids, c.n_cams, c.img, c.img)
-    lang = synth_inputs.lang_ids(obs_seed, ids, c.n_lang, c.vocab)
-    d_img = torch.from_numpy(img).cuda()
-    d_lang = torch.from_numpy(lang).cuda()
-    tok = torch.empty((n, c.n_action_tokens), dtype=torch.int32, device="cuda")
-    act = torch.empty((n, c.n_action_tokens), dtype=torch.float32, device="cuda")
-
-    def step():
-        pol.prefill(ids, images=d_img, lang_ids=d_lang)
-        pol.decode_actions(ids, tokens=tok, actions=act, margins=None, with_margin=False)
-
+    w = Workload(args.workload, E, torch, args.steps + args.warmup)
+    pol, c = w.pol, w.c
     for _ in range(args.warmup):
-        step()
+        w.step()
     torch.cuda.synchronize()
 
-    # ---- timed region: K steps; the dominant kernel class is timed live
-    dominant = E.K_GEMM
+    # ---- untimed pre-pass: which kernel class dominates this workload
+    classes = list(E.KERNEL_CLASSES)
+    pol.profile_enable(classes)
+    for _ in range(2):
+        w.step()
+    pol.profile_enable([])
+    pre = {cls: pol.profile_read(cls, reset=True) for cls in classes}
+    dominant = max(classes, key=lambda k: pre[k]["ms"])
+
+    # ---- timed region: K steps; the dominant kernel class timed live with HIP events
     pol.profile_read(dominant, reset=True)
     pol.profile_enable([dominant])
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     ev0.record(stream)
+    actions = 0
     for _ in range(args.steps):
-        step()
+        actions += w.step()
     ev1.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     pol.profile_enable([])
-    gemm = pol.profile_read(dominant, reset=True)
+    dom = pol.profile_read(dominant, reset=True)
     gpu_ms = ev0.elapsed_time(ev1)
     ms_per_step = 1000.0 * wall / args.steps
-    actions_per_s = n * args.steps / wall
+    actions_per_s = actions / wall
 
     # ---- breakdown pass (not part of the value): every kernel class, per phase
-    classes = list(E.KERNEL_CLASSES)
     pol.profile_enable(classes)
-    phase = {"prefill": 0.0, "decode": 0.0}
+    phase = {"prefill": 0.0, "head": 0.0}
     pe = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
     reps = max(3, min(args.steps, 10))
     for _ in range(reps):
         pe[0].record(stream)
-        pol.prefill(ids, images=d_img, lang_ids=d_lang)
+        if args.workload != "ragged-7b":
+            w.prefill()
         pe[1].record(stream)
-        pol.decode_actions(ids, tokens=tok, actions=act, margins=None, with_margin=False)
+        if args.workload != "ragged-7b":
+            w.head()
+        else:
+            w.step()
         pe[2].record(stream)
         torch.cuda.synchronize()
         phase["prefill"] += pe[0].elapsed_time(pe[1]) / reps
-        phase["decode"] += pe[1].elapsed_time(pe[2]) / reps
+        phase["head"] += pe[1].elapsed_time(pe[2]) / reps
     pol.profile_enable([])
     kernels = {}
     for cls, name in E.KERNEL_CLASSES.items():
@@ -154,21 +235,62 @@ def main():
                              "tflops": round(r["flop"] / (r["ms"] * 1e9), 1) if r["ms"] else None,
                              "gbs": round(r["bytes"] / (r["ms"] * 1e6), 1) if r["ms"] else None}
 
+    # ---- optional: the same steps on CU-masked partitions (the stand-in for SM quotas)
+    partitions = None
+    if args.partitions:
+        partitions = {"1.00": round(actions_per_s, 2)}
+        for q in (1, 2, 3):
+            s_ptr = E.create_cu_masked_stream(0, balanced_mask(q))
+            try:
+                pol.bind_stream(s_ptr)
+                if args.workload == "ragged-7b":
+                    w.call_i = args.warmup
+                torch.cuda.synchronize()
+                t0 = time.perf_counter()
+                n_act = sum(w.step() for _ in range(args.steps))
+                torch.cuda.synchronize()
+                partitions[f"{q / 4:.2f}"] = round(n_act / (time.perf_counter() - t0), 2)
+            finally:
+                pol.bind_stream(stream.cuda_stream)
+                torch.cuda.synchronize()
+                E.destroy_stream(s_ptr)
+
     bf16 = pol.bf16
-    peak = PEAK_BF16_TFLOPS if bf16 else PEAK_FP32_TFLOPS
-    achieved = gemm["flop"] / (gemm["ms"] * 1e9) if gemm["ms"] else 0.0
-    roofline = {"bound": "mfma", "achieved": round(achieved, 1), "peak": peak, "unit": "TFLOP/s",
-                "frac": round(achieved / peak, 4), "traffic": None,
-                "kernel": "gemm_bf16_big_kernel (prefill projections, M >= 256)",
-                "launches": gemm["launches"], "avg_launch_us": round(1000 * gemm["ms"] / max(1, gemm["launches"]), 2),
-                "flop_per_launch": round(gemm["flop"] / max(1, gemm["launches"])),
-                "share_of_step": round(gemm["ms"] / gpu_ms, 3) if gpu_ms else None}
+    if dominant in (E.K_GEMM, E.K_ATTN_PREFILL):
+        peak = PEAK_BF16_TFLOPS if bf16 else PEAK_FP32_TFLOPS
+        achieved = dom["flop"] / (dom["ms"] * 1e9) if dom["ms"] else 0.0
+        roofline = {"bound": "mfma", "achieved": round(achieved, 1), "peak": peak, "unit": "TFLOP/s"}
+        per_launch = {"flop_per_launch": round(dom["flop"] / max(1, dom["launches"]))}
+    else:
+        achieved = dom["bytes"] / (dom["ms"] * 1e6) if dom["ms"] else 0.0
+        roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s"}
+        per_launch = {"bytes_per_launch": round(dom["bytes"] / max(1, dom["launches"]))}
+    roofline.update({"frac": round(achieved / roofline["peak"], 4), "traffic": None,
+                     "kernel": {E.K_GEMM: "gemm_bf16_big_kernel (projections, M >= 256)",
+                                E.K_GEMM_SKINNY: "gemm_bf16_kernel split-K + reduce (decode projections)",
+                                E.K_ATTN_PREFILL: "attn_prefill_bf16_kernel",
+                                E.K_ATTN_DECODE: "attn_decode_split_kernel + combine",
+                                E.K_OTHER: "row-wise kernels"}[dominant],
+                     "launches": dom["launches"],
+                     "avg_launch_us": round(1000 * dom["ms"] / max(1, dom["launches"]), 2),
+                     "share_of_step": round(dom["ms"] / gpu_ms, 3) if gpu_ms else None})
+    roofline.update(per_launch)
 
     base = None
-    if args.cpu_sample > 0:
+    if args.cpu_sample > 0 and args.workload != "ragged-7b":
         log("timing the CPU oracle ...")
-        base = cpu_baseline(preset, obs_seed, args.cpu_sample)
+        base = cpu_baseline(args.workload, args.cpu_sample)
 
+    preset, n, _ = WORKLOADS[args.workload]
+    if args.workload == "ragged-7b":
+        desc = (f"ragged-7b: preset 3 (7B-class), pool of 128 language-only prefixes (T ~ U[200, 320]), "
+                f"{args.steps} decode calls of n ~ U[1, 128] envs")
+    elif c.exp_layers:
+        desc = (f"{args.workload}: preset {preset}, {n} envs, prefix {c.max_seq} tokens, {c.layers}-layer "
+                f"d={c.d} backbone + {c.n_steps} Euler steps of the {c.exp_layers}-layer expert, chunk {c.chunk}x{c.adim}")
+    else:
+        desc = (f"{args.workload}: preset {preset}, {n} envs, prefix {c.max_seq} tokens, {c.layers}-layer "
+                f"d={c.d} decoder, prefill + {c.n_action_tokens - 1} decode steps")
     out = {
         "metric": "policy actions/sec at 1 GPU",
         "value": round(actions_per_s, 2),
@@ -182,17 +304,15 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16" if bf16 else "f32",
         "data": "synthetic (seeded uniform pixels and token ids; random-init N(0, 0.02) weights)",
-        "config": {"workload": f"{args.workload}: preset {preset}, {n} envs, prefix {c.max_seq} tokens, "
-                               f"{c.layers}-layer d={c.d} decoder, prefill + {c.n_action_tokens - 1} decode steps",
-                   "envs": n, "prefix_len": c.max_seq, "layers": c.layers, "d": c.d,
-                   "action_tokens": c.n_action_tokens},
-        "tokens_per_s": round(actions_per_s * c.n_action_tokens, 1),
+        "config": {"workload": desc, "envs": n, "prefix_len": c.max_seq, "layers": c.layers, "d": c.d},
         "gpu_ms_per_step": round(gpu_ms / args.steps, 3),
         "phases_ms": {k: round(v, 3) for k, v in phase.items()},
         "kernels": kernels,
         "roofline": roofline,
         "cpu_baseline": base,
     }
+    if partitions:
+        out["partitions_actions_per_s"] = partitions
     print(json.dumps(out), flush=True)
     pol.close()
 
