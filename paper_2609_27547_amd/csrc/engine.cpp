@@ -11,6 +11,8 @@
 #include <string.h>
 
 #include <algorithm>
+#include <functional>
+#include <map>
 #include <mutex>
 #include <numeric>
 #include <string>
@@ -90,7 +92,6 @@ struct ebrl_policy {
     size_t rows_cap = 0;
     float* X = nullptr;        // residual stream
     void* Xn = nullptr;        // normed rows (act dtype)
-    float* QKV = nullptr;
     void* Qb = nullptr;
     void* Ob = nullptr;
     void* Hb = nullptr;
@@ -122,6 +123,12 @@ struct ebrl_policy {
     double p_ms[EBRL_K_COUNT] = {}, p_flop[EBRL_K_COUNT] = {}, p_bytes[EBRL_K_COUNT] = {};
     int cur_cls = -1;
     hipEvent_t cur_a = nullptr;
+
+    // HIP graphs of whole decode / denoise calls, keyed by the call's shape
+    // and output pointers (the per-call metadata lives at fixed offsets of
+    // meta_dev and is refreshed by an async copy before each launch)
+    hipStream_t cap_stream = nullptr;
+    std::map<std::vector<uint64_t>, hipGraphExec_t> graphs;
 
     std::vector<void*> allocs;
 };
@@ -268,12 +275,21 @@ struct Placement {
     int buf_rows = 0;        // rows of that buffer
     int ld = 0;              // its row length (elements)
     int rows = 0, cols = 0;  // logical shape
-    int kind = 0;            // 0 plain rows at row_off, 1 gate rows, 2 up rows
+    int kind = 0;            // 0 plain rows at row_off, 1 gate rows, 2 up rows,
+                             // 3 rotary-paired rows inside heads of hd rows
     int row_off = 0;
+    int hd = 0;
     bool ok = false;
     int dev_row(int i) const {
         if (kind == 1) return (i / 16) * 32 + (i % 16);
         if (kind == 2) return (i / 16) * 32 + 16 + (i % 16);
+        if (kind == 3) {
+            // head-local row e: first-half rows e < hd/2 and their rotation
+            // partners e + hd/2 interleave in 16-row blocks
+            const int h = i / hd, e = i % hd, half = hd / 2;
+            const int pe = e < half ? (e / 16) * 32 + (e % 16) : ((e - half) / 16) * 32 + 16 + ((e - half) % 16);
+            return row_off + h * hd + pe;
+        }
         return row_off + i;
     }
 };
@@ -309,9 +325,11 @@ Placement placement(const ebrl_policy* p, uint32_t tid) {
     const LayerW& w = (*layers)[l];
     const int qn = sd->hq * sd->hd, kn = sd->hkv * sd->hd, qkvn = qn + 2 * kn;
     switch (slot) {
-    case SLOT_Q: plain(w.qkv, qn, sd->d, sd->d); pl.buf_rows = qkvn; return pl;
-    case SLOT_K: plain(w.qkv, kn, sd->d, sd->d); pl.buf_rows = qkvn; pl.row_off = qn; return pl;
-    case SLOT_V: plain(w.qkv, kn, sd->d, sd->d); pl.buf_rows = qkvn; pl.row_off = qn + kn; return pl;
+    case SLOT_Q: plain(w.qkv, qn, sd->d, sd->d); pl.buf_rows = qkvn; pl.kind = 3; pl.hd = sd->hd; return pl;
+    case SLOT_K: plain(w.qkv, kn, sd->d, sd->d); pl.buf_rows = qkvn; pl.row_off = qn; pl.kind = 3; pl.hd = sd->hd; return pl;
+    case SLOT_V:
+        plain(w.qkv, kn, sd->d, sd->d); pl.buf_rows = qkvn; pl.row_off = qn + kn; pl.kind = 3; pl.hd = sd->hd;
+        return pl;
     case SLOT_O: plain(w.o, sd->d, qn, qn); return pl;
     case SLOT_GATE: plain(w.gu, sd->mlp, sd->d, sd->d); pl.buf_rows = 2 * sd->mlp; pl.kind = 1; return pl;
     case SLOT_UP: plain(w.gu, sd->mlp, sd->d, sd->d); pl.buf_rows = 2 * sd->mlp; pl.kind = 2; return pl;
@@ -417,7 +435,8 @@ int run_gemm(ebrl_policy* p, GemmArgs a, bool split_ok = false) {
     prof_begin(p, cls);
     ebrl::gemm(a, p->stream);
     const double flop = 2.0 * a.M * (double)a.N * a.K;
-    const double outb = a.epi == EPI_SWIGLU ? (double)a.M * a.N / 2 * p->esz : (double)a.M * a.N * 4;
+    const double outb = (a.epi == EPI_SWIGLU ? (double)a.M * a.N / 2 : (double)a.M * a.N) *
+                        (a.epi == EPI_SWIGLU || a.epi == EPI_QKV ? p->esz : 4);
     prof_end(p, flop, ((double)a.M * a.K + (double)a.N * a.K) * p->esz + outb);
     return EBRL_OK;
 }
@@ -445,17 +464,16 @@ int run_block(ebrl_policy* p, BlockCall& b) {
     prof_begin(p, EBRL_K_OTHER);
     rmsnorm_rows(p->bf16, b.R, s.d, nullptr, p->Xn, s.d, b.rows, s.d, 1e-6f, p->stream);
     prof_end(p, 0, (double)b.rows * s.d * (4 + p->esz));
-    GemmArgs g;
-    g.A = p->Xn; g.lda = s.d; g.B = b.w->qkv; g.ldb = s.d; g.M = b.rows; g.N = qkvn; g.K = s.d;
-    g.epi = EPI_F32; g.C = p->QKV; g.ldc = qkvn;
-    run_gemm(p, g, b.decode);
+    // fused QKV projection: rotary embedding of Q and K and the paged K/V
+    // write happen in the GEMM epilogue
     RopeKVArgs r;
-    r.bf16 = p->bf16; r.qkv = p->QKV; r.ld = qkvn; r.M = b.rows; r.q_heads = s.hq;
+    r.bf16 = p->bf16; r.M = b.rows; r.q_heads = s.hq;
     r.Q = p->Qb; r.ldq = qn; r.kv = b.kv; r.seq_env = b.seq_env; r.row_seq = b.row_seq;
     r.row_pos = b.row_pos; r.cos_tab = p->cos_tab; r.sin_tab = p->sin_tab; r.use_rope = b.use_rope;
-    prof_begin(p, EBRL_K_OTHER);
-    rope_kv_write(r, p->stream);
-    prof_end(p, 0, (double)b.rows * qkvn * (4 + p->esz));
+    GemmArgs g;
+    g.A = p->Xn; g.lda = s.d; g.B = b.w->qkv; g.ldb = s.d; g.M = b.rows; g.N = qkvn; g.K = s.d;
+    g.epi = EPI_QKV; g.rope = &r;
+    run_gemm(p, g, b.decode);
     if (b.decode) {
         b.dec.bf16 = p->bf16; b.dec.Q = p->Qb; b.dec.ldq = qn; b.dec.O = p->Ob; b.dec.ldo = qn;
         b.dec.q_heads = s.hq; b.dec.kv = b.kv; b.dec.part = p->part;
@@ -520,6 +538,41 @@ PagedKV dec_kv(const ebrl_policy* p, int layer) {
     return k;
 }
 
+// Enqueue `body` on the bound stream as a cached HIP graph, unless per-kernel
+// timing is on for a kernel class the body launches (`classes`, a bit mask):
+// then it runs eagerly so that every launch can be bracketed by events.
+// `body` launches kernels on p->stream only.
+int run_graph(ebrl_policy* p, const std::vector<uint64_t>& key, int classes, const std::function<int()>& body) {
+    if (p->prof && (p->prof_mask & classes)) return body();
+    auto it = p->graphs.find(key);
+    if (it == p->graphs.end()) {
+        if (p->graphs.size() >= 512) {
+            HIPCHK(p, hipStreamSynchronize(p->stream));
+            for (auto& kv : p->graphs) (void)hipGraphExecDestroy(kv.second);
+            p->graphs.clear();
+        }
+        hipStream_t bound = p->stream;
+        p->stream = p->cap_stream;
+        HIPCHK(p, hipStreamBeginCapture(p->cap_stream, hipStreamCaptureModeRelaxed));
+        int rc = body();
+        hipGraph_t graph = nullptr;
+        hipError_t e = hipStreamEndCapture(p->cap_stream, &graph);
+        p->stream = bound;
+        if (rc) {
+            if (graph) (void)hipGraphDestroy(graph);
+            return rc;
+        }
+        if (e != hipSuccess) return fail(p, EBRL_E_HIP, "graph capture: %s", hipGetErrorString(e));
+        hipGraphExec_t exec = nullptr;
+        e = hipGraphInstantiate(&exec, graph, nullptr, nullptr, 0);
+        (void)hipGraphDestroy(graph);
+        if (e != hipSuccess) return fail(p, EBRL_E_HIP, "graph instantiate: %s", hipGetErrorString(e));
+        it = p->graphs.emplace(key, exec).first;
+    }
+    HIPCHK(p, hipGraphLaunch(it->second, p->stream));
+    return EBRL_OK;
+}
+
 }  // namespace
 
 // =================================================================== ABI ==
@@ -575,6 +628,8 @@ void ebrl_policy_destroy(ebrl_policy* p) {
     (void)hipStreamSynchronize(p->stream);
     for (auto& r : p->recs) { (void)hipEventDestroy(r.a); (void)hipEventDestroy(r.b); }
     for (auto e : p->ev_pool) (void)hipEventDestroy(e);
+    for (auto& kv : p->graphs) (void)hipGraphExecDestroy(kv.second);
+    if (p->cap_stream) (void)hipStreamDestroy(p->cap_stream);
     if (p->meta_ev) (void)hipEventDestroy(p->meta_ev);
     if (p->meta_host) (void)hipHostFree(p->meta_host);
     for (void* a : p->allocs) (void)hipFree(a);
@@ -725,7 +780,6 @@ int ebrl_policy_create(const ebrl_config* config, uint64_t seed, ebrl_policy** o
     const size_t R = p->rows_cap;
     if ((rc = dev_alloc_t(p, &p->X, R * w_d))) return bail(rc);
     if ((rc = dev_alloc(p, &p->Xn, R * w_d * p->esz))) return bail(rc);
-    if ((rc = dev_alloc_t(p, &p->QKV, R * w_qkv))) return bail(rc);
     if ((rc = dev_alloc(p, &p->Qb, R * w_q * p->esz))) return bail(rc);
     if ((rc = dev_alloc(p, &p->Ob, R * w_q * p->esz))) return bail(rc);
     if ((rc = dev_alloc(p, &p->Hb, R * w_mlp * p->esz))) return bail(rc);
@@ -771,6 +825,10 @@ int ebrl_policy_create(const ebrl_config* config, uint64_t seed, ebrl_policy** o
     }
     if (hipEventCreateWithFlags(&p->meta_ev, hipEventDisableTiming) != hipSuccess) {
         fail(p, EBRL_E_HIP, "hipEventCreate failed");
+        return bail(EBRL_E_HIP);
+    }
+    if (hipStreamCreateWithFlags(&p->cap_stream, hipStreamNonBlocking) != hipSuccess) {
+        fail(p, EBRL_E_HIP, "hipStreamCreate failed");
         return bail(EBRL_E_HIP);
     }
     HIPCHK(p, hipDeviceSynchronize());
@@ -984,36 +1042,46 @@ int ebrl_decode_actions(ebrl_policy* p, const int32_t* env_ids, int32_t n, int32
     if ((rc = upload_meta(p, m, false, &md))) return rc;
     const int max_splits = (maxT + steps + ATTN_DEC_CHUNK - 1) / ATTN_DEC_CHUNK;
 
-    LogitsArgs la;
-    la.bf16 = p->bf16; la.W = p->w_act; la.d = c.d; la.n_bins = c.n_bins; la.n = n;
-    la.tokens = out_tokens; la.actions = out_actions; la.margins = out_margin; la.ntok = ntok;
-    la.X = p->h_pre; la.ldx = c.d; la.rows = md + o_env; la.col = 0;
-    prof_begin(p, EBRL_K_OTHER);
-    action_logits(la, p->stream);
-    prof_end(p, 0, (double)c.n_bins * c.d * p->esz);
-    for (int k = 1; k <= steps; ++k) {
-        prof_begin(p, EBRL_K_OTHER);
-        embed_rows(p->bf16, p->e_act, c.n_bins, c.d, out_tokens, nullptr, ntok, k - 1, nullptr, p->X, c.d, n, p->stream);
-        prof_end(p, 0, 0);
-        double kv_bytes = 0;
-        for (int i = 0; i < n; ++i) kv_bytes += (double)(p->envs[env_ids[i]].T + k);
-        kv_bytes *= 2.0 * c.kv_heads * c.head_dim * p->esz;
-        for (int l = 0; l < c.layers; ++l) {
-            BlockCall b;
-            b.R = p->X; b.rows = n; b.sd = &p->dec; b.w = &p->L_dec[l]; b.kv = dec_kv(p, l);
-            b.seq_env = md + o_env; b.row_seq = md + o_id; b.row_pos = md + o_pos + (size_t)(k - 1) * n;
-            b.decode = true;
-            b.dec.seq_env = md + o_env; b.dec.kv_len = md + o_kvl + (size_t)(k - 1) * n; b.dec.n = n;
-            b.dec.max_splits = max_splits;
-            b.attn_bytes = kv_bytes;
-            b.attn_flop = kv_bytes / p->esz / (2.0 * c.kv_heads * c.head_dim) * 4.0 * c.q_heads * c.head_dim;
-            if ((rc = run_block(p, b))) return rc;
-        }
-        la.X = p->X; la.rows = nullptr; la.col = k;
+    auto body = [&]() -> int {
+        LogitsArgs la;
+        la.bf16 = p->bf16; la.W = p->w_act; la.d = c.d; la.n_bins = c.n_bins; la.n = n;
+        la.tokens = out_tokens; la.actions = out_actions; la.margins = out_margin; la.ntok = ntok;
+        la.X = p->h_pre; la.ldx = c.d; la.rows = md + o_env; la.col = 0;
         prof_begin(p, EBRL_K_OTHER);
         action_logits(la, p->stream);
         prof_end(p, 0, (double)c.n_bins * c.d * p->esz);
-    }
+        for (int k = 1; k <= steps; ++k) {
+            prof_begin(p, EBRL_K_OTHER);
+            embed_rows(p->bf16, p->e_act, c.n_bins, c.d, out_tokens, nullptr, ntok, k - 1, nullptr, p->X, c.d, n,
+                       p->stream);
+            prof_end(p, 0, 0);
+            double kv_bytes = 0;
+            for (int i = 0; i < n; ++i) kv_bytes += (double)(p->envs[env_ids[i]].T + k);
+            kv_bytes *= 2.0 * c.kv_heads * c.head_dim * p->esz;
+            for (int l = 0; l < c.layers; ++l) {
+                BlockCall b;
+                b.R = p->X; b.rows = n; b.sd = &p->dec; b.w = &p->L_dec[l]; b.kv = dec_kv(p, l);
+                b.seq_env = md + o_env; b.row_seq = md + o_id; b.row_pos = md + o_pos + (size_t)(k - 1) * n;
+                b.decode = true;
+                b.dec.seq_env = md + o_env; b.dec.kv_len = md + o_kvl + (size_t)(k - 1) * n; b.dec.n = n;
+                b.dec.max_splits = max_splits;
+                b.attn_bytes = kv_bytes;
+                b.attn_flop = kv_bytes / p->esz / (2.0 * c.kv_heads * c.head_dim) * 4.0 * c.q_heads * c.head_dim;
+                int rc2 = run_block(p, b);
+                if (rc2) return rc2;
+            }
+            la.X = p->X; la.rows = nullptr; la.col = k;
+            prof_begin(p, EBRL_K_OTHER);
+            action_logits(la, p->stream);
+            prof_end(p, 0, (double)c.n_bins * c.d * p->esz);
+        }
+        return check_launch(p);
+    };
+    const std::vector<uint64_t> key = {1, (uint64_t)n, (uint64_t)max_splits, (uint64_t)(uintptr_t)out_tokens,
+                                       (uint64_t)(uintptr_t)out_actions, (uint64_t)(uintptr_t)out_margin};
+    const int inside = (1 << EBRL_K_GEMM_SKINNY) | (1 << EBRL_K_ATTN_DECODE) | (1 << EBRL_K_OTHER) |
+                       (n >= 256 ? (1 << EBRL_K_GEMM) : 0);
+    if ((rc = run_graph(p, key, inside, body))) return rc;
     return check_launch(p);
 }
 
@@ -1044,35 +1112,44 @@ int ebrl_flow_denoise(ebrl_policy* p, const int32_t* env_ids, int32_t n, const f
                  o_tq0 = m.add(tq0);
     int* md = nullptr;
     if ((rc = upload_meta(p, m, false, &md))) return rc;
-    // time-MLP outputs for the fixed tau schedule
-    prof_begin(p, EBRL_K_OTHER);
-    small_linear(p->bf16, p->temb, c.n_steps, c.exp_d, p->w_t1, c.exp_d, p->tmid, false, p->stream);
-    small_linear(p->bf16, p->tmid, c.n_steps, c.exp_d, p->w_t2, c.exp_d, p->tvec, true, p->stream);
-    copy_f32(noise, p->flow_x, (size_t)rows * c.adim, p->stream);
-    prof_end(p, 0, 0);
-    for (int k = 0; k < c.n_steps; ++k) {
+    auto body = [&]() -> int {
+        // time-MLP outputs for the fixed tau schedule
         prof_begin(p, EBRL_K_OTHER);
-        flow_in(p->bf16, p->flow_x, rows, c.adim, p->w_ain, p->tvec + (size_t)k * c.exp_d, c.exp_d, p->X, c.exp_d,
-                p->stream);
+        small_linear(p->bf16, p->temb, c.n_steps, c.exp_d, p->w_t1, c.exp_d, p->tmid, false, p->stream);
+        small_linear(p->bf16, p->tmid, c.n_steps, c.exp_d, p->w_t2, c.exp_d, p->tvec, true, p->stream);
+        copy_f32(noise, p->flow_x, (size_t)rows * c.adim, p->stream);
         prof_end(p, 0, 0);
-        for (int l = 0; l < c.exp_layers; ++l) {
-            BlockCall b;
-            b.R = p->X; b.rows = rows; b.sd = &p->exp; b.w = &p->L_exp[l]; b.kv = dec_kv(p, l);
-            b.seq_env = md + o_env; b.row_seq = md + o_rseq; b.row_pos = md + o_rpos;
-            b.pre.seq_env = md + o_env; b.pre.q_off = md + o_off; b.pre.q_len = md + o_len;
-            b.pre.q_pos0 = md + o_pos0; b.pre.kv_len = md + o_kvl; b.pre.tile_seq = md + o_tseq;
-            b.pre.tile_q0 = md + o_tq0; b.pre.n_tiles = (int)tseq.size(); b.pre.causal = false;
-            b.pre.max_kv_len = maxkv;
-            b.attn_flop = 0;
-            for (int i = 0; i < n; ++i) b.attn_flop += 4.0 * c.head_dim * p->exp.hq * (double)c.chunk * kv_len[i];
-            if ((rc = run_block(p, b))) return rc;
+        for (int k = 0; k < c.n_steps; ++k) {
+            prof_begin(p, EBRL_K_OTHER);
+            flow_in(p->bf16, p->flow_x, rows, c.adim, p->w_ain, p->tvec + (size_t)k * c.exp_d, c.exp_d, p->X,
+                    c.exp_d, p->stream);
+            prof_end(p, 0, 0);
+            for (int l = 0; l < c.exp_layers; ++l) {
+                BlockCall b;
+                b.R = p->X; b.rows = rows; b.sd = &p->exp; b.w = &p->L_exp[l]; b.kv = dec_kv(p, l);
+                b.seq_env = md + o_env; b.row_seq = md + o_rseq; b.row_pos = md + o_rpos;
+                b.pre.seq_env = md + o_env; b.pre.q_off = md + o_off; b.pre.q_len = md + o_len;
+                b.pre.q_pos0 = md + o_pos0; b.pre.kv_len = md + o_kvl; b.pre.tile_seq = md + o_tseq;
+                b.pre.tile_q0 = md + o_tq0; b.pre.n_tiles = (int)tseq.size(); b.pre.causal = false;
+                b.pre.max_kv_len = maxkv;
+                b.attn_flop = 0;
+                for (int i = 0; i < n; ++i) b.attn_flop += 4.0 * c.head_dim * p->exp.hq * (double)c.chunk * kv_len[i];
+                int rc2 = run_block(p, b);
+                if (rc2) return rc2;
+            }
+            prof_begin(p, EBRL_K_OTHER);
+            flow_out(p->bf16, p->X, c.exp_d, rows, c.exp_d, p->w_aout, c.adim, 1e-6f, (float)c.n_steps, p->flow_x,
+                     k == 0 ? p->flow_v0 : nullptr, p->stream);
+            prof_end(p, 0, 0);
         }
-        prof_begin(p, EBRL_K_OTHER);
-        flow_out(p->bf16, p->X, c.exp_d, rows, c.exp_d, p->w_aout, c.adim, 1e-6f, (float)c.n_steps, p->flow_x,
-                 k == 0 ? p->flow_v0 : nullptr, p->stream);
-        prof_end(p, 0, 0);
-    }
-    copy_f32(p->flow_x, out_actions, (size_t)rows * c.adim, p->stream);
+        copy_f32(p->flow_x, out_actions, (size_t)rows * c.adim, p->stream);
+        return check_launch(p);
+    };
+    const std::vector<uint64_t> key = {2, (uint64_t)n, (uint64_t)maxkv, (uint64_t)(uintptr_t)noise,
+                                       (uint64_t)(uintptr_t)out_actions};
+    const int inside = (1 << EBRL_K_GEMM) | (1 << EBRL_K_GEMM_SKINNY) | (1 << EBRL_K_ATTN_PREFILL) |
+                       (1 << EBRL_K_OTHER);
+    if ((rc = run_graph(p, key, inside, body))) return rc;
     p->last_flow_ids.assign(env_ids, env_ids + n);
     return check_launch(p);
 }

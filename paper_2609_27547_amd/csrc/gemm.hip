@@ -63,6 +63,52 @@ template <typename T> struct EpiSwiGLU {
     }
 };
 
+// Paired epilogue of the fused QKV projection: columns n (first half of a
+// head-local 32-row group) and n + 16 hold rotation partners e and e + hd/2.
+template <typename T> struct EpiQKV {
+    T* Q; int ldq; T* kv; const int* bt; int bt_stride; int hq, hkv, hd;
+    const int* seq_env; const int* row_seq; const int* row_pos;
+    const float* cos_tab; const float* sin_tab; int use_rope;
+    EBRL_DEV void pair(int m, int n, const float* x1, const float* x2) const {
+        const int qn = hq * hd, kn = hkv * hd;
+        const int region = n < qn ? 0 : (n < qn + kn ? 1 : 2);
+        const int local = n - (region == 0 ? 0 : (region == 1 ? qn : qn + kn));
+        const int h = local / hd, pc = local - h * hd;
+        const int e = (pc >> 5) * 16 + (pc & 15);
+        const int half = hd >> 1;
+        const int pos = row_pos[m];
+        float a[4], b[4];
+#pragma unroll
+        for (int t = 0; t < 4; ++t) { a[t] = x1[t]; b[t] = x2[t]; }
+        if (region < 2 && use_rope) {
+            const float* ct = cos_tab + (size_t)pos * half + e;
+            const float* st = sin_tab + (size_t)pos * half + e;
+#pragma unroll
+            for (int t = 0; t < 4; ++t) {
+                const float c = ct[t], sn = st[t];
+                a[t] = x1[t] * c - x2[t] * sn;
+                b[t] = x2[t] * c + x1[t] * sn;
+            }
+        }
+        T* dst;
+        if (region == 0) {
+            dst = Q + (size_t)m * ldq + h * hd;
+        } else {
+            const int env = seq_env[row_seq[m]];
+            const int blk = bt[(size_t)env * bt_stride + (pos >> 4)];
+            dst = kv + (size_t)blk * 2 * hkv * KV_BLOCK * hd + ((size_t)(region == 2 ? hkv : 0) + h) * KV_BLOCK * hd +
+                  (size_t)(pos & 15) * hd;
+        }
+        st4<T>(dst + e, a[0], a[1], a[2], a[3]);
+        st4<T>(dst + e + half, b[0], b[1], b[2], b[3]);
+    }
+};
+template <typename T> EpiQKV<T> make_epi_qkv(const RopeKVArgs& r) {
+    return EpiQKV<T>{(T*)r.Q, r.ldq, (T*)r.kv.base, r.kv.block_table, r.kv.bt_stride, r.q_heads,
+                     r.kv.kv_heads, r.kv.head_dim, r.seq_env, r.row_seq, r.row_pos, r.cos_tab, r.sin_tab,
+                     (int)r.use_rope};
+}
+
 // ------------------------------------------------------- bf16 MFMA GEMM --
 
 constexpr int BK = 64;
@@ -606,6 +652,9 @@ int gemm(const GemmArgs& a, hipStream_t s) {
     case EPI_SWIGLU:
         if (a.bf16) return dispatch<true>(a, EpiSwiGLU<bf16_t>{(bf16_t*)a.C, a.ldc}, s);
         return dispatch<true>(a, EpiSwiGLU<float>{(float*)a.C, a.ldc}, s);
+    case EPI_QKV:
+        if (a.bf16) return dispatch<true>(a, make_epi_qkv<bf16_t>(*a.rope), s);
+        return dispatch<true>(a, make_epi_qkv<float>(*a.rope), s);
     }
     return 0;
 }

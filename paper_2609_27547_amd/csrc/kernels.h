@@ -15,8 +15,10 @@ enum EpiKind {
     EPI_ACT = 1,     // C act dtype = acc (bf16 or f32)
     EPI_RESID = 2,   // C f32 += acc (residual stream)
     EPI_REMAP = 3,   // C f32 row row_base[m/group] + m%group = acc (+ add row m%group)
-    EPI_SWIGLU = 4   // packed gate/up -> C act [M, N/2] = silu(gate) * up
+    EPI_SWIGLU = 4,  // packed gate/up -> C act [M, N/2] = silu(gate) * up
+    EPI_QKV = 5      // rotary-paired Q/K/V rows -> rotated Q (act) + paged K/V cache (see RopeKVArgs)
 };
+struct RopeKVArgs;
 
 struct GemmArgs {
     bool bf16 = true;
@@ -27,6 +29,7 @@ struct GemmArgs {
     void* C = nullptr; int ldc = 0;
     const int* row_base = nullptr; int group = 1;
     const void* add = nullptr; int add_ld = 0;
+    const RopeKVArgs* rope = nullptr;           // EPI_QKV parameters
     float* ws = nullptr; size_t ws_floats = 0;  // split-K workspace
     // Decode GEMMs (M = batch, at most 256) may split K; the split count then
     // depends on (N, K) only, so an element's summation order -- and its bits
@@ -92,9 +95,12 @@ void attn_decode(const AttnDecodeArgs& a, hipStream_t s);
 void rmsnorm_rows(bool bf16_out, const float* X, int ldx, const int* rows, void* Y, int ldy,
                   int n_rows, int d, float eps, hipStream_t s);
 
-// Split the fused QKV projection (f32, [M, (hq + 2 hkv) hd]) into rotated
-// queries (act dtype) and rotated keys + values written to the paged cache
-// at (seq_env[row_seq[m]], row_pos[m]).  use_rope = false skips rotation.
+// Rotary embedding + paged KV write of the fused QKV projection, applied in
+// the GEMM epilogue (EPI_QKV): rotated queries go to Q (act dtype), rotated
+// keys and the values to the paged cache at (seq_env[row_seq[m]],
+// row_pos[m]).  use_rope = false skips rotation.  The QKV weight rows are
+// packed per head so that rows e and e + hd/2 sit in the two 16-row halves
+// of one 32-row group.  (qkv/ld are used only by the standalone kernel.)
 struct RopeKVArgs {
     bool bf16 = true;
     const float* qkv = nullptr; int ld = 0;
