@@ -258,7 +258,8 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(
 
 
 // ------------------------------------------------ bf16 MFMA GEMM, large M --
-// 256-row macro tiles, 4 waves in 2 x 2, each wave a 128 x (BN/2) tile.
+// 256 x 256 macro tiles, 16 waves in 4 x 4 (64 x 64 per wave, four waves
+// per SIMD so that one wave's LDS waits overlap another's MFMAs).
 // Operands go global -> LDS with global_load_lds_dwordx4 (no VGPR staging):
 // a wave instruction writes 64 lanes x 16 bytes contiguously, so the tile is
 // stored as 16-byte chunks, chunk (row, c) of a 64-element row at position
@@ -409,6 +410,7 @@ __global__ __launch_bounds__(64 * WM * WN, 1) void gemm_bf16_big_kernel(
         }
     }
 }
+
 
 // ------------------------------------------------------------ fp32 GEMM --
 // 64 x 64 tile, BK 16, 256 threads; thread (ty, tx) owns rows 2ty, 2ty+1 and
@@ -570,7 +572,7 @@ static void launch_bf16(const GemmArgs& a, const GemmPlan& p, Epi epi, hipStream
     const bool split = p.splits > 1;
     if (p.big) {
         dim3 grid(((a.M + 255) / 256) * ((a.N + 255) / 256), 1);
-        hipLaunchKernelGGL((gemm_bf16_big_kernel<256, 2, 4, PAIRED, false, Epi>), grid, dim3(512), 0, s,
+        hipLaunchKernelGGL((gemm_bf16_big_kernel<256, 4, 4, PAIRED, false, Epi>), grid, dim3(1024), 0, s,
                            (const bf16_t*)a.A, a.lda, (const bf16_t*)a.B, a.ldb, a.M, a.N, a.K, a.K, a.ws, epi);
         return;
     }
