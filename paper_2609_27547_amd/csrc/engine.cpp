@@ -101,6 +101,7 @@ struct ebrl_policy {
     float* h_norm = nullptr;
     float* ws = nullptr;       // split-K workspace
     size_t ws_floats = 0;
+    unsigned* counters = nullptr;  // split-K tile counters (zero between calls)
     float* part = nullptr;     // decode attention partials
     size_t part_floats = 0;
     float* flow_x = nullptr;
@@ -431,6 +432,7 @@ int run_gemm(ebrl_policy* p, GemmArgs a, bool split_ok = false) {
     a.split_ok = split_ok;
     a.ws = p->ws;
     a.ws_floats = p->ws_floats;
+    a.counters = p->counters;
     const int cls = a.M >= 256 ? EBRL_K_GEMM : EBRL_K_GEMM_SKINNY;
     prof_begin(p, cls);
     ebrl::gemm(a, p->stream);
@@ -803,6 +805,8 @@ int ebrl_policy_create(const ebrl_config* config, uint64_t seed, ebrl_policy** o
     // split-K workspace: 16 splits of the widest skinny projection
     p->ws_floats = (size_t)16 * 256 * std::max(w_qkv, 2 * w_mlp);
     if ((rc = dev_alloc_t(p, &p->ws, p->ws_floats))) return bail(rc);
+    if ((rc = dev_alloc_t(p, &p->counters, ebrl::gemm_counter_words()))) return bail(rc);
+    HIPCHK(p, hipMemset(p->counters, 0, ebrl::gemm_counter_words() * 4));
     const int max_splits = (c.max_seq + p->tail + ATTN_DEC_CHUNK - 1) / ATTN_DEC_CHUNK;
     p->part_floats = (size_t)c.max_envs * c.q_heads * max_splits * (c.head_dim + 2);
     if ((rc = dev_alloc_t(p, &p->part, p->part_floats))) return bail(rc);
@@ -1287,14 +1291,18 @@ int ebrl_op_gemm(int32_t dtype, const void* A, const void* B, float* C, int32_t 
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess) return EBRL_E_HIP;
     if (!g_ws || g_ws_dev != dev) {
-        g_ws_floats = (size_t)16 << 20;  // 64 MB, kept for the process lifetime
-        if (hipMalloc((void**)&g_ws, g_ws_floats * 4) != hipSuccess) { g_ws = nullptr; return EBRL_E_OOM; }
+        // 64 MB of partials plus the tile counters, kept for the process lifetime
+        g_ws_floats = (size_t)16 << 20;
+        const size_t words = g_ws_floats + ebrl::gemm_counter_words();
+        if (hipMalloc((void**)&g_ws, words * 4) != hipSuccess) { g_ws = nullptr; return EBRL_E_OOM; }
+        if (hipMemset(g_ws + g_ws_floats, 0, ebrl::gemm_counter_words() * 4) != hipSuccess) return EBRL_E_HIP;
         g_ws_dev = dev;
     }
     GemmArgs a;
     a.bf16 = dtype == EBRL_DTYPE_BF16;
     a.A = A; a.lda = K; a.B = B; a.ldb = K; a.M = M; a.N = N; a.K = K;
     a.epi = EPI_F32; a.C = C; a.ldc = N; a.ws = g_ws; a.ws_floats = g_ws_floats;
+    a.counters = reinterpret_cast<unsigned*>(g_ws + g_ws_floats);
     a.split_ok = M < 256;
     ebrl::gemm(a, (hipStream_t)stream);
     return hipGetLastError() == hipSuccess ? EBRL_OK : EBRL_E_HIP;

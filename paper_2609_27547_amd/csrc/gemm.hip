@@ -412,6 +412,272 @@ __global__ __launch_bounds__(64 * WM * WN, 1) void gemm_bf16_big_kernel(
 }
 
 
+// ------------------------------------------- bf16 GEMM, decode-sized M --
+// M <= 256 (one row per environment), K % 64 == 0.  A workgroup owns a
+// 64-column slice of the output, at most 64 rows (further row tiles in more
+// workgroups) and a contiguous range of 64-wide K groups; the range is the
+// whole K unless the column slices alone are too few to occupy the chip.  The
+// four waves split that range and run independent pipelines: each wave
+// streams its weight and activation rows into its own LDS region with
+// global_load_lds_dwordx4 (one instruction = 8 rows x 128 contiguous bytes,
+// whole cache lines), two buffers deep, and multiplies from LDS.  Loading
+// whole 128-byte row segments per instruction roughly doubles the rate a CU
+// sustains compared with loading 16 rows x 64 bytes straight into MFMA
+// register layout.  The waves' tiles are summed in wave order through LDS.
+// With several K splits each workgroup stores its partial tile, and the
+// workgroup that finishes a tile last (a device-scope counter per tile) sums
+// the partials in split order, runs the epilogue and clears the counter for
+// the next call.  An element's summation order depends only on (N, K).
+constexpr int DEC_BN = 64;
+constexpr int DEC_MAX_SPLITS = 16;
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+
+// Buffer accesses with the device-coherence cache policy bit (sc1): they
+// bypass the per-XCD L2s, the same policy the compiler uses for agent-scope
+// atomic loads and stores, so partial tiles written by one XCD are read
+// correctly by another without cache-wide write-back or invalidation.
+constexpr int CPOL_SC1 = 16;
+EBRL_DEV __amdgpu_buffer_rsrc_t coherent_rsrc(float* base) {
+    return __builtin_amdgcn_make_buffer_rsrc(base, 0, 0x7fffffff, 0x00020000);
+}
+EBRL_DEV void st_coherent4(__amdgpu_buffer_rsrc_t r, int byte_off, f32x4 v) {
+    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), r, byte_off, 0, CPOL_SC1);
+}
+EBRL_DEV f32x4 ld_coherent4(__amdgpu_buffer_rsrc_t r, int byte_off) {
+    return __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(r, byte_off, 0, CPOL_SC1));
+}
+constexpr int DEC_TILE_FLOATS = 64 * 64;   // partial-tile stride in the workspace
+constexpr int DEC_MAX_COUNTERS = 4096;
+
+// s_waitcnt on the vector-memory counter only (gfx9 encoding: expcnt and
+// lgkmcnt fields at their maxima).
+template <int N> EBRL_DEV void wait_vmcnt() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt((N & 15) | 0x70 | 0xF00 | ((N >> 4) << 14));
+}
+
+// One wave's DMA of ROWS rows x 64 bf16 (K group k0) into `lds`: row q of the
+// group sits in instruction q / 8, lane (q % 8) * 8 + (c ^ (q % 8)) holds its
+// 16-byte chunk c (the XOR spreads a fragment read over the banks).  Issued
+// as inline assembly, so the compiler neither counts these loads nor guards
+// LDS reads against them: the caller waits on vmcnt itself (each wave reads
+// only the region its own DMA fills).
+EBRL_DEV void dma16_to_lds(const void* g, uint32_t lds_addr) {
+    asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+                 :: "v"(g), "s"(lds_addr) : "memory", "m0");
+}
+template <int ROWS>
+EBRL_DEV void dec_dma(const bf16_t* __restrict__ G, int ld, int row0, int rows_valid, int k0, bf16_t* lds,
+                      int lane) {
+    const int q = lane >> 3, c = (lane & 7) ^ q;
+    const uint32_t base = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(lds_ptr_t)lds);
+#pragma unroll
+    for (int t = 0; t < ROWS / 8; ++t) {
+        const int gr = min(row0 + t * 8 + q, rows_valid - 1);
+        dma16_to_lds(G + (size_t)gr * ld + k0 + c * 8, base + t * 1024);
+    }
+}
+EBRL_DEV bf16x8 dec_frag(const bf16_t* lds, int row, int c) {
+    return *reinterpret_cast<const bf16x8*>(lds + (row >> 3) * 512 + ((row & 7) * 8 + (c ^ (row & 7))) * 8);
+}
+
+template <int TM, bool PAIRED, class Epi>
+__global__ __launch_bounds__(256) void gemm_bf16_decode_kernel(
+    const bf16_t* __restrict__ A, int lda, const bf16_t* __restrict__ W, int ldw, int M, int N,
+    int K, int groups_per_split, int splits, int m_tiles, float* __restrict__ ws,
+    unsigned* __restrict__ counters, Epi epi)
+{
+    constexpr int TN = DEC_BN / 16;
+    constexpr int FR = TM * TN;            // output fragments per wave
+    constexpr int WE = DEC_BN * 64;        // bf16 per wave per buffer: weights
+    constexpr int XE = TM * 16 * 64;       //                             activations
+    constexpr int NDMA = (DEC_BN + TM * 16) / 8;   // DMA instructions per K group
+    // one __shared__ object per buffer and operand, so that the compiler can
+    // tell the buffer being read from the one the DMA is filling
+    __shared__ __attribute__((aligned(1024))) bf16_t sW0[4 * WE];
+    __shared__ __attribute__((aligned(1024))) bf16_t sX0[4 * XE];
+    __shared__ __attribute__((aligned(1024))) bf16_t sW1[4 * WE];
+    __shared__ __attribute__((aligned(1024))) bf16_t sX1[4 * XE];
+    __shared__ int s_last;
+    static_assert(4 * FR * 64 * 16 <= (int)(sizeof(sW0) + sizeof(sX0)), "reduction buffer");
+
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int r = lane & 15, g = lane >> 4;
+    const int tiles_n = (N + DEC_BN - 1) / DEC_BN;
+    // XCD-aware order: the row tiles of one (column slice, split) pair --
+    // which read the same weights -- run on the same XCD.
+    int bid = blockIdx.x;
+    const int nb = gridDim.x;
+    if ((nb & 7) == 0) bid = (bid & 7) * (nb >> 3) + (bid >> 3);
+    const int mt = bid % m_tiles;
+    const int unit = bid / m_tiles;
+    const int split = unit % splits, nt = unit / splits;
+    const int m0 = mt * 16 * TM, n0 = nt * DEC_BN;
+    const int kgroups = K >> 6;
+    const int s_begin = split * groups_per_split;
+    const int s_end = min(kgroups, s_begin + groups_per_split);
+    const int gpw = (groups_per_split + 3) >> 2;
+    const int w_begin = min(s_end, s_begin + wave * gpw);
+    const int w_end = min(s_end, w_begin + gpw);
+
+    bf16_t* const w0 = sW0 + wave * WE; bf16_t* const x0 = sX0 + wave * XE;
+    bf16_t* const w1 = sW1 + wave * WE; bf16_t* const x1 = sX1 + wave * XE;
+    auto dma = [&](int grp, bf16_t* wl, bf16_t* xl) {
+        dec_dma<DEC_BN>(W, ldw, n0, N, grp * 64, wl, lane);
+        dec_dma<TM * 16>(A, lda, m0, M, grp * 64, xl, lane);
+    };
+
+    f32x4 acc[TM][TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    // both 32-wide steps of a K group: fragment reads first, then the MFMAs
+    auto compute = [&](const bf16_t* wl, const bf16_t* xl) {
+        bf16x8 wa[2][TN], xb[2][TM];
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+#pragma unroll
+            for (int j = 0; j < TN; ++j) wa[u][j] = dec_frag(wl, j * 16 + r, u * 4 + g);
+#pragma unroll
+            for (int i = 0; i < TM; ++i) xb[u][i] = dec_frag(xl, i * 16 + r, u * 4 + g);
+        }
+#pragma unroll
+        for (int u = 0; u < 2; ++u)
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+#pragma unroll
+                for (int j = 0; j < TN; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wa[u][j], xb[u][i], acc[i][j], 0, 0, 0);
+    };
+
+    if (w_begin < w_end) {
+        dma(w_begin, w0, x0);
+        for (int gi = w_begin; gi < w_end; gi += 2) {
+            if (gi + 1 < w_end) {
+                dma(gi + 1, w1, x1);
+                wait_vmcnt<NDMA>();
+            } else {
+                wait_vmcnt<0>();
+            }
+            compute(w0, x0);
+            if (gi + 1 >= w_end) break;
+            if (gi + 2 < w_end) {
+                dma(gi + 2, w0, x0);
+                wait_vmcnt<NDMA>();
+            } else {
+                wait_vmcnt<0>();
+            }
+            compute(w1, x1);
+        }
+    }
+
+    // waves' tiles through LDS (the staging buffers, once every wave is done)
+    __syncthreads();
+    f32x4* red = (wave * FR * 64 * 16 < (int)sizeof(sW0))
+                     ? reinterpret_cast<f32x4*>(sW0) + wave * FR * 64
+                     : reinterpret_cast<f32x4*>(sX0) + (wave * FR * 64 - (int)sizeof(sW0) / 16);
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) red[(i * TN + j) * 64 + lane] = acc[i][j];
+    __syncthreads();
+    auto red_at = [&](int w, int e) -> f32x4 {
+        const int idx = w * FR * 64 + e;
+        return idx * 16 < (int)sizeof(sW0) ? reinterpret_cast<const f32x4*>(sW0)[idx]
+                                            : reinterpret_cast<const f32x4*>(sX0)[idx - (int)sizeof(sW0) / 16];
+    };
+
+    // Output units: one fragment lane (or a gate/up fragment pair) each.
+    constexpr int G = PAIRED ? 2 : 1;
+    constexpr int UNITS = FR / G * 64;
+    constexpr int PER = (UNITS + 255) / 256;
+    f32x4 v[PER][G];
+#pragma unroll
+    for (int q = 0; q < PER; ++q) {
+        const int u = tid + 256 * q;
+        if (u < UNITS) {
+            const int f0 = (u >> 6) * G, l = u & 63;
+#pragma unroll
+            for (int h = 0; h < G; ++h) {
+                const int e = (f0 + h) * 64 + l;
+                v[q][h] = ((red_at(0, e) + red_at(1, e)) + red_at(2, e)) + red_at(3, e);
+            }
+        }
+    }
+
+    if (splits > 1) {
+        // A workgroup waits for its own partial stores to complete before it
+        // bumps the counter; the last one reads the partials only after
+        // seeing the final count.
+        const int tile = nt * m_tiles + mt;
+        const __amdgpu_buffer_rsrc_t part =
+            coherent_rsrc(ws + (size_t)tile * splits * DEC_TILE_FLOATS);
+#pragma unroll
+        for (int q = 0; q < PER; ++q) {
+            const int u = tid + 256 * q;
+            if (u < UNITS) {
+                const int f0 = (u >> 6) * G, l = u & 63;
+#pragma unroll
+                for (int h = 0; h < G; ++h)
+                    st_coherent4(part, (split * DEC_TILE_FLOATS + ((f0 + h) * 64 + l) * 4) * 4, v[q][h]);
+            }
+        }
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        __syncthreads();
+        if (tid == 0)
+            s_last = __hip_atomic_fetch_add(counters + tile, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
+                     (unsigned)(splits - 1);
+        __syncthreads();
+        if (!s_last) return;
+        // all splits' loads in flight at once, then summed in split order
+#pragma unroll
+        for (int q = 0; q < PER; ++q) {
+            const int u = tid + 256 * q;
+            if (u < UNITS) {
+                const int f0 = (u >> 6) * G, l = u & 63;
+#pragma unroll
+                for (int h = 0; h < G; ++h) {
+                    const int off = ((f0 + h) * 64 + l) * 16;
+                    f32x4 t[DEC_MAX_SPLITS];
+#pragma unroll
+                    for (int sp = 0; sp < DEC_MAX_SPLITS; ++sp)
+                        t[sp] = ld_coherent4(part, min(sp, splits - 1) * DEC_TILE_FLOATS * 4 + off);
+                    f32x4 acc_t = t[0];
+#pragma unroll
+                    for (int sp = 1; sp < DEC_MAX_SPLITS; ++sp)
+                        if (sp < splits) acc_t += t[sp];
+                    v[q][h] = acc_t;
+                }
+            }
+        }
+        if (tid == 0) __hip_atomic_store(counters + tile, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+
+#pragma unroll
+    for (int q = 0; q < PER; ++q) {
+        const int u = tid + 256 * q;
+        if (u < UNITS) {
+            const int fg = u >> 6, l = u & 63;
+            const int f0 = fg * G;
+            const int i = f0 / TN, j = f0 - i * TN;
+            const int m = m0 + i * 16 + (l & 15);
+            const int n = n0 + j * 16 + 4 * (l >> 4);
+            if (m < M && n < N) {
+                if constexpr (PAIRED) {
+                    float gv[4] = {v[q][0][0], v[q][0][1], v[q][0][2], v[q][0][3]};
+                    float uv[4] = {v[q][1][0], v[q][1][1], v[q][1][2], v[q][1][3]};
+                    epi.pair(m, n, gv, uv);
+                } else {
+                    epi(m, n, v[q][0][0], v[q][0][1], v[q][0][2], v[q][0][3]);
+                }
+            }
+        }
+    }
+}
+
+
 // ------------------------------------------------------------ fp32 GEMM --
 // 64 x 64 tile, BK 16, 256 threads; thread (ty, tx) owns rows 2ty, 2ty+1 and
 // columns grp*32 + q*4 + {0..3} and the same +16 (tx = grp*4 + q), so that a
@@ -527,7 +793,10 @@ __global__ void splitk_reduce_kernel(const float* __restrict__ ws, int splits, i
 // ------------------------------------------------------------- dispatch --
 
 // Tile and split choice depend only on (M, N, K).
-struct GemmPlan { int bm; int bn; int splits; int k_per_split; bool big; };
+struct GemmPlan {
+    int bm; int bn; int splits; int k_per_split; bool big;
+    bool dec; int steps_per_split; int tm; int m_tiles;   // decode kernel (steps: 64-wide K groups)
+};
 
 // Kernel and split choice.  The tile variant never changes an element's
 // summation order; the split count (decode only) is a function of (N, K).
@@ -536,9 +805,34 @@ constexpr int SPLIT_MAX_M = 256;
 static GemmPlan plan_gemm(bool bf16, int M, int N, int K, size_t ws_floats, bool split_ok) {
     GemmPlan p;
     p.big = false;
+    p.dec = false;
     p.bn = 0;
     p.splits = 1;
     p.k_per_split = K;
+    if (bf16 && split_ok && K % 64 == 0) {
+        // About 128 workgroups from column slices x K splits, a split at
+        // least 16 K groups (1024 wide): the cross-workgroup hand-off costs
+        // about as much as streaming that much more per workgroup.  The
+        // partial tiles of up to four row tiles must fit the workspace.
+        p.dec = true;
+        const int tiles_n = (N + DEC_BN - 1) / DEC_BN;
+        const int kgroups = K / 64;
+        const int want = std::max(1, std::min({(128 + tiles_n - 1) / tiles_n, kgroups / 16, DEC_MAX_SPLITS}));
+        int gps = (kgroups + want - 1) / want;
+        for (;;) {
+            const int sp = (kgroups + gps - 1) / gps;
+            if (sp == 1) break;
+            if (sp <= DEC_MAX_SPLITS && (size_t)sp * 4 * tiles_n * DEC_TILE_FLOATS <= ws_floats &&
+                4 * tiles_n <= DEC_MAX_COUNTERS)
+                break;
+            ++gps;
+        }
+        p.steps_per_split = gps;
+        p.splits = (kgroups + gps - 1) / gps;
+        p.tm = M <= 16 ? 1 : (M <= 32 ? 2 : 4);
+        p.m_tiles = (M + 16 * p.tm - 1) / (16 * p.tm);
+        return p;
+    }
     if (bf16 && !split_ok && M >= 256 && K % 64 == 0) {
         p.big = true;
         p.bm = 256;
@@ -574,6 +868,19 @@ static void launch_bf16(const GemmArgs& a, const GemmPlan& p, Epi epi, hipStream
         dim3 grid(((a.M + 255) / 256) * ((a.N + 255) / 256), 1);
         hipLaunchKernelGGL((gemm_bf16_big_kernel<256, 4, 4, PAIRED, false, Epi>), grid, dim3(1024), 0, s,
                            (const bf16_t*)a.A, a.lda, (const bf16_t*)a.B, a.ldb, a.M, a.N, a.K, a.K, a.ws, epi);
+        return;
+    }
+    if (p.dec) {
+        const int tiles_n = (a.N + DEC_BN - 1) / DEC_BN;
+        dim3 grid(tiles_n * p.splits * p.m_tiles);
+        auto godec = [&](auto kern) {
+            hipLaunchKernelGGL(kern, grid, dim3(256), 0, s, (const bf16_t*)a.A, a.lda, (const bf16_t*)a.B,
+                               a.ldb, a.M, a.N, a.K, p.steps_per_split, p.splits, p.m_tiles, a.ws,
+                               a.counters, epi);
+        };
+        if (p.tm == 1) godec(gemm_bf16_decode_kernel<1, PAIRED, Epi>);
+        else if (p.tm == 2) godec(gemm_bf16_decode_kernel<2, PAIRED, Epi>);
+        else godec(gemm_bf16_decode_kernel<4, PAIRED, Epi>);
         return;
     }
     auto go = [&](auto kern, int bm, int bn) {
@@ -629,7 +936,8 @@ static void launch_f32(const GemmArgs& a, const GemmPlan& p, Epi epi, hipStream_
 
 template <bool PAIRED, class Epi>
 static int dispatch(const GemmArgs& a, Epi epi, hipStream_t s) {
-    const GemmPlan p = plan_gemm(a.bf16, a.M, a.N, a.K, a.ws_floats, a.split_ok && a.M <= SPLIT_MAX_M);
+    const GemmPlan p = plan_gemm(a.bf16, a.M, a.N, a.K, a.ws_floats,
+                                 a.split_ok && a.M <= SPLIT_MAX_M && (!a.bf16 || a.counters));
     if (a.bf16) launch_bf16<PAIRED>(a, p, epi, s);
     else launch_f32<PAIRED>(a, p, epi, s);
     return p.splits;
@@ -663,6 +971,10 @@ int gemm(const GemmArgs& a, hipStream_t s) {
 
 int gemm_splits(bool bf16, int M, int N, int K, size_t ws_floats, bool split_ok) {
     return plan_gemm(bf16, M, N, K, ws_floats, split_ok && M <= SPLIT_MAX_M).splits;
+}
+
+size_t gemm_counter_words() {
+    return DEC_MAX_COUNTERS;
 }
 
 }  // namespace ebrl

@@ -31,6 +31,9 @@ struct GemmArgs {
     const void* add = nullptr; int add_ld = 0;
     const RopeKVArgs* rope = nullptr;           // EPI_QKV parameters
     float* ws = nullptr; size_t ws_floats = 0;  // split-K workspace
+    // gemm_counter_words() zeroed words; bf16 GEMMs with K splits leave them
+    // zero again.  Calls that share a workspace must not overlap in time.
+    unsigned* counters = nullptr;
     // Decode GEMMs (M = batch, at most 256) may split K; the split count then
     // depends on (N, K) only, so an element's summation order -- and its bits
     // -- do not depend on the batch size.  Without splitting, every kernel
@@ -41,6 +44,7 @@ struct GemmArgs {
 // Returns the number of K splits used (1 = single pass).
 int gemm(const GemmArgs& a, hipStream_t s);
 int gemm_splits(bool bf16, int M, int N, int K, size_t ws_floats, bool split_ok);
+size_t gemm_counter_words();
 
 // ------------------------------------------------------------- attention --
 // Paged KV: layer base pointer; physical block b holds

@@ -44,7 +44,8 @@ def _ebrl_config(o: M.Config, max_envs: int, max_seq: int = 0) -> "E.Config":
 
 @pytest.mark.parametrize("M_,N,K", [(1, 64, 64), (16, 256, 64), (17, 128, 72), (64, 3072, 1024),
                                     (100, 192, 1024), (300, 1024, 512), (513, 384, 768), (40, 8192, 1024),
-                                    (700, 2304, 256), (1100, 4096, 640)])
+                                    (700, 2304, 256), (1100, 4096, 640), (255, 1024, 4096), (8, 4100, 11008),
+                                    (33, 100, 96)])
 @pytest.mark.parametrize("dtype", ["bf16", "fp32"])
 def test_gemm_matches_oracle_linear(M_, N, K, dtype):
     rng = np.random.default_rng(M_ * 7 + N + K)
@@ -63,6 +64,28 @@ def test_gemm_matches_oracle_linear(M_, N, K, dtype):
     torch.cuda.synchronize()
     ref = M.linear(a64, b64)
     assert P.row_rel_err(C.cpu().numpy(), ref) < 2e-6
+
+
+@pytest.mark.parametrize("N,K", [(3072, 1024), (1024, 4096), (4096, 11008)])
+def test_decode_gemm_repeat_and_row_subsets_bitwise(N, K):
+    """Decode-sized GEMMs split K across workgroups; the per-tile completion
+    counters must be back at zero after each call (a repeated call gives the
+    same bits), and a row's result must not depend on how many rows the call
+    holds (batch invariance)."""
+    rng = np.random.default_rng(N + K)
+    A = torch.from_numpy(rng.normal(size=(200, K)).astype(np.float32)).to(torch.bfloat16).cuda()
+    B = torch.from_numpy(rng.normal(size=(N, K)).astype(np.float32)).to(torch.bfloat16).cuda()
+    full = torch.empty((200, N), dtype=torch.float32, device="cuda")
+    again = torch.empty_like(full)
+    E.op_gemm(A, B, full)
+    E.op_gemm(A, B, again)
+    torch.cuda.synchronize()
+    assert torch.equal(full, again)
+    for m in [1, 7, 16, 17, 40, 64, 130]:
+        C = torch.empty((m, N), dtype=torch.float32, device="cuda")
+        E.op_gemm(A[:m].contiguous(), B, C)
+        torch.cuda.synchronize()
+        assert torch.equal(C, full[:m]), m
 
 
 # ------------------------------------------------------- resident weights --
