@@ -339,6 +339,118 @@ __global__ __launch_bounds__(256) void attn_decode_split_kernel(AttnDecodeArgs a
     if (tid == 0) { part[HD] = sml[0]; part[HD + 1] = sml[1]; }
 }
 
+// bf16 decode attention, one workgroup per (sequence, query head) over the
+// whole cache.  The four waves take consecutive quarters of the keys; a wave
+// loads 8 K rows and the matching 8 V rows per round in one burst (a load
+// instruction covers whole 128-byte row segments: 8 keys of 64 dims or 4
+// keys of 128), keeps a running max / sum / weighted V per lane, and the
+// waves' results are merged through LDS in wave order.  The key split
+// depends only on the sequence length, so a sequence's output does not
+// depend on the rest of the batch.
+constexpr int DEC_BT_MAX = 256;   // block-table entries staged in LDS (4096 tokens)
+
+template <int HD>
+__global__ __launch_bounds__(256) void attn_decode_bf16_kernel(AttnDecodeArgs a, float scale_log2)
+{
+    constexpr int LPK = HD / 8;        // lanes per key row, 16 bytes each
+    constexpr int KPL = 64 / LPK;      // keys per wave load
+    constexpr int NL = 8;              // K (and V) loads per lane per round
+    constexpr int KW = KPL * NL;       // keys per round
+    __shared__ int s_bt[DEC_BT_MAX];
+    __shared__ float s_o[4][HD];
+    __shared__ float s_ml[4][2];
+
+    const int i = blockIdx.x, h = blockIdx.y;
+    const int kvlen = a.kv_len[i];
+    const int env = a.seq_env[i];
+    const int hkv = a.kv.kv_heads;
+    const int kvh = h / (a.q_heads / hkv);
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int sub = lane % LPK, kq = lane / LPK;
+    const int nblk = (kvlen + KV_BLOCK - 1) / KV_BLOCK;
+    for (int b = tid; b < nblk; b += 256) s_bt[b] = a.kv.block_table[(size_t)env * a.kv.bt_stride + b];
+    float q[8];
+    load8<bf16_t>((const bf16_t*)a.Q + (size_t)i * a.ldq + h * HD + sub * 8, q);
+    __syncthreads();
+
+    const int per = (kvlen + 3) / 4;
+    const int wb = min(kvlen, wave * per), we = min(kvlen, wb + per);
+    const size_t blk_elems = (size_t)2 * hkv * KV_BLOCK * HD;
+    const bf16_t* kbase = (const bf16_t*)a.kv.base + (size_t)kvh * KV_BLOCK * HD + sub * 8;
+    const bf16_t* vbase = kbase + (size_t)hkv * KV_BLOCK * HD;
+
+    float m_run = -INFINITY, l_run = 0.f, acc[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) acc[j] = 0.f;
+    for (int kb = wb; kb < we; kb += KW) {
+        uint4 kr[NL], vr[NL];
+#pragma unroll
+        for (int t = 0; t < NL; ++t) {
+            const int key = min(kb + t * KPL + kq, we - 1);
+            const size_t off = (size_t)s_bt[key >> 4] * blk_elems + (size_t)(key & 15) * HD;
+            kr[t] = *reinterpret_cast<const uint4*>(kbase + off);
+            vr[t] = *reinterpret_cast<const uint4*>(vbase + off);
+        }
+        float sc[NL];
+        float mr = -INFINITY;
+#pragma unroll
+        for (int t = 0; t < NL; ++t) {
+            float kv[8];
+            load8<bf16_t>(reinterpret_cast<const bf16_t*>(&kr[t]), kv);
+            float dot = 0.f;
+#pragma unroll
+            for (int j = 0; j < 8; ++j) dot = fmaf(q[j], kv[j], dot);
+#pragma unroll
+            for (int off = LPK / 2; off > 0; off >>= 1) dot += __shfl_xor(dot, off, 64);
+            sc[t] = (kb + t * KPL + kq < we) ? dot * scale_log2 : -INFINITY;
+            mr = fmaxf(mr, sc[t]);
+        }
+        mr = wave_max(mr);
+        const float m_new = fmaxf(m_run, mr);
+        const float alpha = (m_run == -INFINITY) ? 0.f : fast_exp2(m_run - m_new);
+        l_run *= alpha;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) acc[j] *= alpha;
+#pragma unroll
+        for (int t = 0; t < NL; ++t) {
+            const float p = (sc[t] == -INFINITY) ? 0.f : fast_exp2(sc[t] - m_new);
+            l_run += p;
+            float vv[8];
+            load8<bf16_t>(reinterpret_cast<const bf16_t*>(&vr[t]), vv);
+#pragma unroll
+            for (int j = 0; j < 8; ++j) acc[j] = fmaf(p, vv[j], acc[j]);
+        }
+        m_run = m_new;
+    }
+    // lanes of one key slot hold the same l; sum over the key slots
+#pragma unroll
+    for (int off = LPK; off < 64; off <<= 1) {
+        l_run += __shfl_xor(l_run, off, 64);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) acc[j] += __shfl_xor(acc[j], off, 64);
+    }
+    if (kq == 0) {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) s_o[wave][sub * 8 + j] = acc[j];
+    }
+    if (lane == 0) { s_ml[wave][0] = m_run; s_ml[wave][1] = l_run; }
+    __syncthreads();
+    if (tid < HD) {
+        float M = -INFINITY;
+#pragma unroll
+        for (int w = 0; w < 4; ++w) M = fmaxf(M, s_ml[w][0]);
+        float L = 0.f, o = 0.f;
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+            const float wt = (s_ml[w][0] == -INFINITY) ? 0.f : fast_exp2(s_ml[w][0] - M);
+            L += wt * s_ml[w][1];
+            o += wt * s_o[w][tid];
+        }
+        st_elem<bf16_t>((bf16_t*)a.O + (size_t)i * a.ldo + h * HD + tid, kvlen > 0 ? o / L : 0.f);
+    }
+}
+
 // grid (n, q_heads), HD threads
 template <typename T, int HD>
 __global__ void attn_decode_combine_kernel(AttnDecodeArgs a)
@@ -362,7 +474,12 @@ void attn_decode(const AttnDecodeArgs& a, hipStream_t s) {
     const int hd = a.kv.head_dim;
     const float scale_log2 = 1.4426950408889634f / sqrtf((float)hd);
     dim3 g1(a.n, a.q_heads, a.max_splits), g2(a.n, a.q_heads);
-    if (a.bf16) {
+    if (a.bf16 && a.kv.bt_stride <= DEC_BT_MAX) {
+        if (hd == 64)
+            hipLaunchKernelGGL(attn_decode_bf16_kernel<64>, g2, dim3(256), 0, s, a, scale_log2);
+        else
+            hipLaunchKernelGGL(attn_decode_bf16_kernel<128>, g2, dim3(256), 0, s, a, scale_log2);
+    } else if (a.bf16) {
         if (hd == 64) {
             hipLaunchKernelGGL((attn_decode_split_kernel<bf16_t, 64>), g1, dim3(256), 0, s, a, scale_log2);
             hipLaunchKernelGGL((attn_decode_combine_kernel<bf16_t, 64>), g2, dim3(64), 0, s, a);
