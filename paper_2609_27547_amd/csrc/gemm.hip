@@ -379,33 +379,47 @@ __global__ __launch_bounds__(64 * WM * WN, 1) void gemm_bf16_big_kernel(
         }
     }
 
+    // Epilogue through LDS (free once every wave has passed the loop's last
+    // barrier): a wave stages 16 rows x 64 columns of its tile at a time and
+    // reads them back row-contiguous, so that each store (and the residual
+    // read) covers 256-byte fp32 / 64-128-byte bf16 row segments instead of
+    // 16-32-byte pieces of 16 rows.  Rows are padded to 68 floats so the
+    // fragment-layout writes spread over the banks.
+    static_assert(!SPLIT, "the large-M kernel never splits K");
+    static_assert(WTN == 64 && NW == 16, "staging assumes 64-column wave tiles, 16 waves");
+    constexpr int SROW = 68;
+    bf16_t* const region = wave < 4 ? sA0 : (wave < 8 ? sA1 : (wave < 12 ? sB0 : sB1));
+    float* const stage = reinterpret_cast<float*>(region) + (wave & 3) * 16 * SROW;
+    const int ncol0 = n0 + wn * WTN;
 #pragma unroll
     for (int i = 0; i < TM; ++i) {
-        const int m = m0 + wm * WTM + i * 16 + r;
-        if (m >= M) continue;
-        if constexpr (SPLIT) {
 #pragma unroll
-            for (int j = 0; j < TN; ++j) {
-                const int n = n0 + wn * WTN + j * 16 + 4 * g;
-                if (n < N)
-                    st4<float>(ws + ((size_t)blockIdx.y * M + m) * N + n, acc[i][j][0], acc[i][j][1],
-                               acc[i][j][2], acc[i][j][3]);
-            }
-        } else if constexpr (PAIRED) {
+        for (int j = 0; j < TN; ++j)
+            *reinterpret_cast<f32x4*>(stage + r * SROW + j * 16 + 4 * g) = acc[i][j];
+        const int mrow0 = m0 + wm * WTM + i * 16;
+        if constexpr (PAIRED) {
+            // 8 lanes per row: gate columns c (c % 32 < 16) with up partner c + 16
 #pragma unroll
-            for (int j = 0; j < TN; j += 2) {
-                const int n = n0 + wn * WTN + j * 16 + 4 * g;
-                if (n < N) {
-                    float gv[4] = {acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]};
-                    float uv[4] = {acc[i][j + 1][0], acc[i][j + 1][1], acc[i][j + 1][2], acc[i][j + 1][3]};
+            for (int pass = 0; pass < 2; ++pass) {
+                const int row = pass * 8 + (lane >> 3);
+                const int c = ((lane >> 2) & 1) * 32 + (lane & 3) * 4;
+                const f32x4 gv4 = *reinterpret_cast<const f32x4*>(stage + row * SROW + c);
+                const f32x4 uv4 = *reinterpret_cast<const f32x4*>(stage + row * SROW + c + 16);
+                const int m = mrow0 + row, n = ncol0 + c;
+                if (m < M && n < N) {
+                    float gv[4] = {gv4[0], gv4[1], gv4[2], gv4[3]};
+                    float uv[4] = {uv4[0], uv4[1], uv4[2], uv4[3]};
                     epi.pair(m, n, gv, uv);
                 }
             }
         } else {
 #pragma unroll
-            for (int j = 0; j < TN; ++j) {
-                const int n = n0 + wn * WTN + j * 16 + 4 * g;
-                if (n < N) epi(m, n, acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]);
+            for (int pass = 0; pass < 4; ++pass) {
+                const int row = pass * 4 + (lane >> 4);
+                const int c = (lane & 15) * 4;
+                const f32x4 v = *reinterpret_cast<const f32x4*>(stage + row * SROW + c);
+                const int m = mrow0 + row, n = ncol0 + c;
+                if (m < M && n < N) epi(m, n, v[0], v[1], v[2], v[3]);
             }
         }
     }
