@@ -22,14 +22,27 @@ namespace ebrl {
 
 // --------------------------------------------------------- bf16 prefill --
 
+typedef __attribute__((address_space(3))) void* attn_lds_ptr_t;
+typedef short attn_v4s __attribute__((ext_vector_type(4)));
+
+// global_load_lds_dwordx4 issued as inline assembly: the compiler neither
+// counts it nor guards LDS reads against it; the kernel waits on vmcnt and
+// synchronises the workgroup itself before reading a filled buffer.
+EBRL_DEV void attn_dma16(const void* g, uint32_t lds_addr) {
+    asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+                 :: "v"(g), "s"(lds_addr) : "memory", "m0");
+}
+
 template <int HD>
 __global__ __launch_bounds__(256) void attn_prefill_bf16_kernel(AttnPrefillArgs a, float scale_log2)
 {
-    constexpr int KT = 64;
-    constexpr int KS = HD + 8;   // sK row stride (bf16)
-    constexpr int VS = KT + 8;   // sVt row stride (bf16)
-    __shared__ __attribute__((aligned(16))) bf16_t sK[KT * KS];
-    __shared__ __attribute__((aligned(16))) bf16_t sVt[HD * VS];
+    constexpr int KT = 64;                 // keys per tile
+    constexpr int CPR = HD / 8;            // 16-byte chunks per K/V row
+    constexpr int RPI = 64 / CPR;          // rows per DMA instruction
+    constexpr int TILE = KT * HD;          // bf16 per K (or V) tile
+    __shared__ __attribute__((aligned(1024))) bf16_t sK[2][TILE];
+    __shared__ __attribute__((aligned(1024))) bf16_t sV[2][TILE];
+    __shared__ int s_bt[ATTN_BT_MAX];
 
     const int t = blockIdx.x, h = blockIdx.y;
     const int seq = a.tile_seq[t], qt0 = a.tile_q0[t];
@@ -38,11 +51,18 @@ __global__ __launch_bounds__(256) void attn_prefill_bf16_kernel(AttnPrefillArgs 
     const int qoff = a.q_off[seq];
     const int hkv = a.kv.kv_heads;
     const int kvh = h / (a.q_heads / hkv);
-    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int r = lane & 15, g = lane >> 4;
     const int qi = qt0 + wave * 16 + r;
     const bool qvalid = qi < qlen;
     const int qpos = qpos0 + qi;
+
+    int kv_end = kvlen;
+    if (a.causal) kv_end = min(kvlen, qpos0 + min(qt0 + 64, qlen));
+    const int ntiles = (kv_end + KT - 1) / KT;
+    for (int b2 = tid; b2 < (kv_end + KV_BLOCK - 1) / KV_BLOCK; b2 += 256)
+        s_bt[b2] = a.kv.block_table[(size_t)env * a.kv.bt_stride + b2];
 
     bf16x8 qb[HD / 32];
     {
@@ -54,49 +74,58 @@ __global__ __launch_bounds__(256) void attn_prefill_bf16_kernel(AttnPrefillArgs 
             qb[ks] = *reinterpret_cast<bf16x8*>(&v);
         }
     }
+    __syncthreads();
 
-    int kv_end = kvlen;
-    if (a.causal) kv_end = min(kvlen, qpos0 + min(qt0 + 64, qlen));
+    // DMA of key tile `it`: row q of the tile = key k0 + q, its 16-byte chunk
+    // c stored at chunk position q * CPR + (c ^ (q & 7)); the waves split the
+    // tile's 64 / RPI instructions for K and the same for V.
+    const size_t blk_elems = (size_t)2 * hkv * KV_BLOCK * HD;
+    const bf16_t* kbase = (const bf16_t*)a.kv.base + (size_t)kvh * KV_BLOCK * HD;
+    const size_t voff = (size_t)hkv * KV_BLOCK * HD;
+    const uint32_t sk_addr = (uint32_t)(uintptr_t)(attn_lds_ptr_t)&sK[0][0];
+    const uint32_t sv_addr = (uint32_t)(uintptr_t)(attn_lds_ptr_t)&sV[0][0];
+    auto dma = [&](int it, int buf) {
+        constexpr int NI = KT / RPI;             // instructions per operand
+        const int row_in = lane / CPR, cpos = lane % CPR;
+#pragma unroll
+        for (int u = 0; u < NI / 4; ++u) {
+            const int ins = wave * (NI / 4) + u;
+            const int q = ins * RPI + row_in;
+            const int key = min(it * KT + q, kv_end - 1);
+            const int c = cpos ^ (q & 7);
+            const bf16_t* src = kbase + (size_t)s_bt[key >> 4] * blk_elems + (size_t)(key & 15) * HD + c * 8;
+            const uint32_t off = (uint32_t)(buf * TILE + ins * 512) * 2;
+            attn_dma16(src, __builtin_amdgcn_readfirstlane(sk_addr + off));
+            attn_dma16(src + voff, __builtin_amdgcn_readfirstlane(sv_addr + off));
+        }
+    };
 
     f32x4 acc[HD / 16];
 #pragma unroll
     for (int i = 0; i < HD / 16; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
     float m_i = -INFINITY, l_i = 0.f;
 
-    const size_t blk_elems = (size_t)2 * hkv * KV_BLOCK * HD;
-    const bf16_t* kvbase = (const bf16_t*)a.kv.base;
-    const int* bt = a.kv.block_table + (size_t)env * a.kv.bt_stride;
-
-    for (int k0 = 0; k0 < kv_end; k0 += KT) {
+    if (ntiles > 0) dma(0, 0);
+    for (int it = 0; it < ntiles; ++it) {
+        // tile `it` has landed for every wave, and every wave is done with
+        // tile it - 1, whose buffer the next DMA refills
+        __builtin_amdgcn_s_waitcnt(0);
         __syncthreads();
-        constexpr int CH = KT * HD / 8;
-#pragma unroll
-        for (int c = tid; c < CH; c += 256) {
-            const int key = c / (HD / 8), dc = (c % (HD / 8)) * 8;
-            const int kidx = k0 + key;
-            uint4 kv = make_uint4(0, 0, 0, 0), vv = make_uint4(0, 0, 0, 0);
-            if (kidx < kvlen) {
-                const int blk = bt[kidx >> 4];
-                const bf16_t* p = kvbase + (size_t)blk * blk_elems +
-                                  ((size_t)kvh * KV_BLOCK + (kidx & 15)) * HD + dc;
-                kv = *reinterpret_cast<const uint4*>(p);
-                vv = *reinterpret_cast<const uint4*>(p + (size_t)hkv * KV_BLOCK * HD);
-            }
-            *reinterpret_cast<uint4*>(&sK[key * KS + dc]) = kv;
-            const bf16_t* ve = reinterpret_cast<const bf16_t*>(&vv);
-#pragma unroll
-            for (int j = 0; j < 8; ++j) sVt[(dc + j) * VS + key] = ve[j];
-        }
-        __syncthreads();
+        if (it + 1 < ntiles) dma(it + 1, (it + 1) & 1);
+        const bf16_t* tk = sK[it & 1];
+        const bf16_t* tv = sV[it & 1];
+        const int k0 = it * KT;
 
         // S^T tiles: lane holds key 16kt + 4g + v for query r
         f32x4 s[4];
 #pragma unroll
         for (int kt = 0; kt < 4; ++kt) {
             s[kt] = f32x4{0.f, 0.f, 0.f, 0.f};
+            const int row = kt * 16 + r;
 #pragma unroll
             for (int ks = 0; ks < HD / 32; ++ks) {
-                const bf16x8 ka = *reinterpret_cast<const bf16x8*>(&sK[(kt * 16 + r) * KS + ks * 32 + g * 8]);
+                const bf16x8 ka =
+                    *reinterpret_cast<const bf16x8*>(tk + (row * CPR + ((ks * 4 + g) ^ (row & 7))) * 8);
                 s[kt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka, qb[ks], s[kt], 0, 0, 0);
             }
         }
@@ -136,6 +165,11 @@ __global__ __launch_bounds__(256) void attn_prefill_bf16_kernel(AttnPrefillArgs 
 #pragma unroll
         for (int i = 0; i < HD / 16; ++i) acc[i] *= alpha;
 
+        // O^T += V^T P^T.  V stays row-major in LDS; ds_read_b64_tr_b16 hands
+        // lane (r, g) the values of dimension 16 dt + r for 4 keys per read
+        // (keys 32 ks2 + 4g + j, then 32 ks2 + 16 + 4g + j), the same key
+        // order the score lanes hold.
+        const int a16 = lane & 15;
 #pragma unroll
         for (int ks2 = 0; ks2 < 2; ++ks2) {
             bf16x8 pb;
@@ -146,12 +180,21 @@ __global__ __launch_bounds__(256) void attn_prefill_bf16_kernel(AttnPrefillArgs 
             }
 #pragma unroll
             for (int dt = 0; dt < HD / 16; ++dt) {
-                const bf16_t* vr = &sVt[(dt * 16 + r) * VS + ks2 * 32 + 4 * g];
-                uint4 w;
-                const uint2 lo = *reinterpret_cast<const uint2*>(vr);
-                const uint2 hi = *reinterpret_cast<const uint2*>(vr + 16);
-                w.x = lo.x; w.y = lo.y; w.z = hi.x; w.w = hi.y;
-                const bf16x8 va = *reinterpret_cast<bf16x8*>(&w);
+                const int d = dt * 16 + 4 * (a16 & 3);
+                attn_v4s lo, hi;
+                {
+                    const int key = 32 * ks2 + 4 * g + (a16 >> 2);
+                    const int off = (key * CPR + ((d >> 3) ^ (key & 7))) * 8 + (d & 7);
+                    lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) attn_v4s*)(attn_lds_ptr_t)(tv + off));
+                }
+                {
+                    const int key = 32 * ks2 + 16 + 4 * g + (a16 >> 2);
+                    const int off = (key * CPR + ((d >> 3) ^ (key & 7))) * 8 + (d & 7);
+                    hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) attn_v4s*)(attn_lds_ptr_t)(tv + off));
+                }
+                const uint2 lo2 = __builtin_bit_cast(uint2, lo), hi2 = __builtin_bit_cast(uint2, hi);
+                const uint4 w = make_uint4(lo2.x, lo2.y, hi2.x, hi2.y);
+                const bf16x8 va = __builtin_bit_cast(bf16x8, w);
                 acc[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, pb, acc[dt], 0, 0, 0);
             }
         }
@@ -226,6 +269,7 @@ void attn_prefill(const AttnPrefillArgs& a, hipStream_t s) {
     if (a.n_tiles <= 0) return;
     const int hd = a.kv.head_dim;
     if (a.bf16) {
+        if (a.kv.bt_stride > ATTN_BT_MAX) return;   // rejected by the caller (capacity check)
         const float scale_log2 = 1.4426950408889634f / sqrtf((float)hd);
         dim3 grid(a.n_tiles, a.q_heads);
         if (hd == 64) hipLaunchKernelGGL(attn_prefill_bf16_kernel<64>, grid, dim3(256), 0, s, a, scale_log2);
@@ -347,7 +391,6 @@ __global__ __launch_bounds__(256) void attn_decode_split_kernel(AttnDecodeArgs a
 // waves' results are merged through LDS in wave order.  The key split
 // depends only on the sequence length, so a sequence's output does not
 // depend on the rest of the batch.
-constexpr int DEC_BT_MAX = 256;   // block-table entries staged in LDS (4096 tokens)
 
 template <int HD>
 __global__ __launch_bounds__(256) void attn_decode_bf16_kernel(AttnDecodeArgs a, float scale_log2)
@@ -356,7 +399,7 @@ __global__ __launch_bounds__(256) void attn_decode_bf16_kernel(AttnDecodeArgs a,
     constexpr int KPL = 64 / LPK;      // keys per wave load
     constexpr int NL = 8;              // K (and V) loads per lane per round
     constexpr int KW = KPL * NL;       // keys per round
-    __shared__ int s_bt[DEC_BT_MAX];
+    __shared__ int s_bt[ATTN_BT_MAX];
     __shared__ float s_o[4][HD];
     __shared__ float s_ml[4][2];
 
@@ -474,7 +517,7 @@ void attn_decode(const AttnDecodeArgs& a, hipStream_t s) {
     const int hd = a.kv.head_dim;
     const float scale_log2 = 1.4426950408889634f / sqrtf((float)hd);
     dim3 g1(a.n, a.q_heads, a.max_splits), g2(a.n, a.q_heads);
-    if (a.bf16 && a.kv.bt_stride <= DEC_BT_MAX) {
+    if (a.bf16 && a.kv.bt_stride <= ATTN_BT_MAX) {
         if (hd == 64)
             hipLaunchKernelGGL(attn_decode_bf16_kernel<64>, g2, dim3(256), 0, s, a, scale_log2);
         else

@@ -422,6 +422,15 @@ int validate(const ebrl_config& c, std::string& why) {
     if (!c.action_logits && !c.exp_layers) return bad("no action head and no expert");
     if (c.max_envs < 1 || c.max_seq < 1) return bad("capacity");
     if (!(c.init_std > 0.0)) return bad("init_std");
+    {
+        // the bf16 attention kernels stage a sequence's block table in LDS
+        const int tail = std::max(c.action_logits ? c.n_action_tokens - 1 : 0, c.exp_layers ? c.chunk : 0);
+        const int blocks = (c.max_seq + tail + KV_BLOCK - 1) / KV_BLOCK;
+        const int vit_blocks =
+            c.n_cams ? (c.n_cams * (c.img / c.patch) * (c.img / c.patch) + KV_BLOCK - 1) / KV_BLOCK : 0;
+        if (c.dtype == EBRL_DTYPE_BF16 && std::max(blocks, vit_blocks) > ATTN_BT_MAX)
+            return bad("sequence too long for the bf16 attention kernels (4096 tokens per sequence)");
+    }
     return EBRL_OK;
 }
 

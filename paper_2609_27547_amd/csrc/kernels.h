@@ -76,6 +76,9 @@ struct AttnPrefillArgs {
     int max_kv_len = 0;             // fp32 path: scores buffer size
 };
 void attn_prefill(const AttnPrefillArgs& a, hipStream_t s);
+// bf16 attention kernels stage a sequence's block table in LDS: at most this
+// many 16-token blocks (4096 tokens) per sequence.
+constexpr int ATTN_BT_MAX = 256;
 
 // One query per sequence against kv_len[i] keys, split over the sequence
 // in chunks of ATTN_DEC_CHUNK keys, then combined in chunk order.
