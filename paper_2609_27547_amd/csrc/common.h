@@ -69,3 +69,29 @@ EBRL_DEV float block_sum(float v, float* red) {
 EBRL_DEV float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
 constexpr int KV_BLOCK = 16;  // tokens per paged-KV block
+
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+
+// Buffer accesses with the device-coherence cache policy bit (sc1): they
+// bypass the per-XCD L2s, the same policy the compiler uses for agent-scope
+// atomic loads and stores, so data one workgroup writes is read correctly by
+// a workgroup on another XCD without cache-wide write-back or invalidation.
+// Used for in-kernel hand-offs: the writer waits for its stores (vmcnt 0)
+// before bumping a device-scope counter; the reader loads after seeing the
+// final count.
+constexpr int CPOL_SC1 = 16;
+EBRL_DEV __amdgpu_buffer_rsrc_t coherent_rsrc(float* base) {
+    return __builtin_amdgcn_make_buffer_rsrc(base, 0, 0x7fffffff, 0x00020000);
+}
+EBRL_DEV void st_coherent4(__amdgpu_buffer_rsrc_t r, int byte_off, f32x4 v) {
+    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), r, byte_off, 0, CPOL_SC1);
+}
+EBRL_DEV f32x4 ld_coherent4(__amdgpu_buffer_rsrc_t r, int byte_off) {
+    return __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(r, byte_off, 0, CPOL_SC1));
+}
+EBRL_DEV void st_coherent1(__amdgpu_buffer_rsrc_t r, int byte_off, float v) {
+    __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, v), r, byte_off, 0, CPOL_SC1);
+}
+EBRL_DEV float ld_coherent1(__amdgpu_buffer_rsrc_t r, int byte_off) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, byte_off, 0, CPOL_SC1));
+}

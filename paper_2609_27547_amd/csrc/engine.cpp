@@ -102,6 +102,8 @@ struct ebrl_policy {
     float* ws = nullptr;       // split-K workspace
     size_t ws_floats = 0;
     unsigned* counters = nullptr;  // split-K tile counters (zero between calls)
+    float* lg = nullptr;           // action logits scratch [max_envs][n_bins]
+    unsigned* lg_counters = nullptr;
     float* part = nullptr;     // decode attention partials
     size_t part_floats = 0;
     float* flow_x = nullptr;
@@ -816,6 +818,11 @@ int ebrl_policy_create(const ebrl_config* config, uint64_t seed, ebrl_policy** o
     if ((rc = dev_alloc_t(p, &p->ws, p->ws_floats))) return bail(rc);
     if ((rc = dev_alloc_t(p, &p->counters, ebrl::gemm_counter_words()))) return bail(rc);
     HIPCHK(p, hipMemset(p->counters, 0, ebrl::gemm_counter_words() * 4));
+    if (c.action_logits) {
+        if ((rc = dev_alloc_t(p, &p->lg, (size_t)c.max_envs * c.n_bins))) return bail(rc);
+        if ((rc = dev_alloc_t(p, &p->lg_counters, (size_t)c.max_envs))) return bail(rc);
+        HIPCHK(p, hipMemset(p->lg_counters, 0, (size_t)c.max_envs * 4));
+    }
     const int max_splits = (c.max_seq + p->tail + ATTN_DEC_CHUNK - 1) / ATTN_DEC_CHUNK;
     p->part_floats = (size_t)c.max_envs * c.q_heads * max_splits * (c.head_dim + 2);
     if ((rc = dev_alloc_t(p, &p->part, p->part_floats))) return bail(rc);
@@ -933,6 +940,9 @@ int ebrl_prefill(ebrl_policy* p, const ebrl_obs_batch* obs, const int32_t* env_i
     std::vector<std::pair<int, int>> tiles;
     for (int i = 0; i < n; ++i)
         for (int q0 = 0; q0 < T[i]; q0 += 64) tiles.push_back({i, q0});
+    // causal tiles late in a sequence see the most keys: dispatch them first
+    std::stable_sort(tiles.begin(), tiles.end(),
+                     [](const std::pair<int, int>& x, const std::pair<int, int>& y) { return x.second > y.second; });
     std::stable_sort(tiles.begin(), tiles.end(), [](auto& a, auto& b) { return a.second > b.second; });
     std::vector<int> tile_seq(tiles.size()), tile_q0(tiles.size());
     for (size_t t = 0; t < tiles.size(); ++t) { tile_seq[t] = tiles[t].first; tile_q0[t] = tiles[t].second; }
@@ -1059,6 +1069,7 @@ int ebrl_decode_actions(ebrl_policy* p, const int32_t* env_ids, int32_t n, int32
         LogitsArgs la;
         la.bf16 = p->bf16; la.W = p->w_act; la.d = c.d; la.n_bins = c.n_bins; la.n = n;
         la.tokens = out_tokens; la.actions = out_actions; la.margins = out_margin; la.ntok = ntok;
+        la.lg = p->lg; la.counters = p->lg_counters;
         la.X = p->h_pre; la.ldx = c.d; la.rows = md + o_env; la.col = 0;
         prof_begin(p, EBRL_K_OTHER);
         action_logits(la, p->stream);

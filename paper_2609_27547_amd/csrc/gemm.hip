@@ -444,22 +444,6 @@ __global__ __launch_bounds__(64 * WM * WN, 1) void gemm_bf16_big_kernel(
 // the next call.  An element's summation order depends only on (N, K).
 constexpr int DEC_BN = 64;
 constexpr int DEC_MAX_SPLITS = 16;
-typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
-
-// Buffer accesses with the device-coherence cache policy bit (sc1): they
-// bypass the per-XCD L2s, the same policy the compiler uses for agent-scope
-// atomic loads and stores, so partial tiles written by one XCD are read
-// correctly by another without cache-wide write-back or invalidation.
-constexpr int CPOL_SC1 = 16;
-EBRL_DEV __amdgpu_buffer_rsrc_t coherent_rsrc(float* base) {
-    return __builtin_amdgcn_make_buffer_rsrc(base, 0, 0x7fffffff, 0x00020000);
-}
-EBRL_DEV void st_coherent4(__amdgpu_buffer_rsrc_t r, int byte_off, f32x4 v) {
-    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), r, byte_off, 0, CPOL_SC1);
-}
-EBRL_DEV f32x4 ld_coherent4(__amdgpu_buffer_rsrc_t r, int byte_off) {
-    return __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(r, byte_off, 0, CPOL_SC1));
-}
 constexpr int DEC_TILE_FLOATS = 64 * 64;   // partial-tile stride in the workspace
 constexpr int DEC_MAX_COUNTERS = 4096;
 

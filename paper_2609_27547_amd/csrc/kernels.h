@@ -143,6 +143,9 @@ struct LogitsArgs {
     float eps = 1e-6f;
     int* tokens = nullptr; float* actions = nullptr; float* margins = nullptr;
     int ntok = 7, col = 0;
+    // bf16 heads with d % 512 == 0 and n_bins % 64 == 0: logits scratch
+    // [n][n_bins] and n zeroed per-row counters (left zero after the call)
+    float* lg = nullptr; unsigned* counters = nullptr;
 };
 void action_logits(const LogitsArgs& a, hipStream_t s);
 

@@ -53,9 +53,54 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(const float* X, int ldx, c
     }
 }
 
+// One wave per row for d % 256 == 0: the row stays in registers (NV float4
+// per lane, lane-interleaved so each load instruction reads 1 KB of the row),
+// the sum of squares is a wave reduction, no workgroup barrier.
+template <typename TO, int NV>
+__global__ __launch_bounds__(256) void rmsnorm_wave_kernel(const float* X, int ldx, const int* rows, TO* Y,
+                                                           int ldy, int n_rows, int d, float eps)
+{
+    const int i = blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (i >= n_rows) return;
+    const int lane = threadIdx.x & 63;
+    const int src = rows ? rows[i] : i;
+    const float* x = X + (size_t)src * ldx;
+    float4 v[NV];
+    float ss = 0.f;
+#pragma unroll
+    for (int k = 0; k < NV; ++k) {
+        v[k] = *reinterpret_cast<const float4*>(x + (k * 64 + lane) * 4);
+        ss += v[k].x * v[k].x + v[k].y * v[k].y + v[k].z * v[k].z + v[k].w * v[k].w;
+    }
+    ss = wave_sum(ss);
+    const float rs = 1.0f / sqrtf(ss / (float)d + eps);
+    TO* y = Y + (size_t)i * ldy;
+#pragma unroll
+    for (int k = 0; k < NV; ++k)
+        st4<TO>(y + (k * 64 + lane) * 4, v[k].x * rs, v[k].y * rs, v[k].z * rs, v[k].w * rs);
+}
+
+template <typename TO>
+static bool rmsnorm_wave(const float* X, int ldx, const int* rows, TO* Y, int ldy, int n_rows, int d,
+                         float eps, hipStream_t s) {
+    if (d % 256) return false;
+    const dim3 grid((n_rows + 3) / 4), block(256);
+    switch (d / 256) {
+    case 1: hipLaunchKernelGGL((rmsnorm_wave_kernel<TO, 1>), grid, block, 0, s, X, ldx, rows, Y, ldy, n_rows, d, eps); return true;
+    case 2: hipLaunchKernelGGL((rmsnorm_wave_kernel<TO, 2>), grid, block, 0, s, X, ldx, rows, Y, ldy, n_rows, d, eps); return true;
+    case 4: hipLaunchKernelGGL((rmsnorm_wave_kernel<TO, 4>), grid, block, 0, s, X, ldx, rows, Y, ldy, n_rows, d, eps); return true;
+    case 8: hipLaunchKernelGGL((rmsnorm_wave_kernel<TO, 8>), grid, block, 0, s, X, ldx, rows, Y, ldy, n_rows, d, eps); return true;
+    case 16: hipLaunchKernelGGL((rmsnorm_wave_kernel<TO, 16>), grid, block, 0, s, X, ldx, rows, Y, ldy, n_rows, d, eps); return true;
+    default: return false;
+    }
+}
+
 void rmsnorm_rows(bool bf16_out, const float* X, int ldx, const int* rows, void* Y, int ldy,
                   int n_rows, int d, float eps, hipStream_t s) {
     if (n_rows <= 0) return;
+    if (bf16_out ? rmsnorm_wave<bf16_t>(X, ldx, rows, (bf16_t*)Y, ldy, n_rows, d, eps, s)
+                 : rmsnorm_wave<float>(X, ldx, rows, (float*)Y, ldy, n_rows, d, eps, s))
+        return;
     if (bf16_out)
         hipLaunchKernelGGL(rmsnorm_kernel<bf16_t>, dim3(n_rows), dim3(256), 0, s, X, ldx, rows,
                            (bf16_t*)Y, ldy, d, eps);
@@ -243,8 +288,90 @@ __global__ __launch_bounds__(256) void logits_kernel(LogitsArgs a)
     }
 }
 
+// bf16 action head, split over bins: grid (row, n_bins / 64).  A workgroup
+// normalises its row (RMSNorm, gains 1) into LDS, each wave takes 16 bins and
+// loads their weight rows in one burst per 512 columns; the row's logits go
+// to a scratch row, and the last of the row's workgroups (device-scope
+// counter) takes the argmax (ties to the lowest bin) and the top-2 margin.
+__global__ __launch_bounds__(256) void logits_split_kernel(LogitsArgs a)
+{
+    extern __shared__ float hn[];   // [d]
+    __shared__ float red[16];
+    __shared__ int s_last;
+    const int i = blockIdx.x, part = blockIdx.y;
+    const int src = a.rows ? a.rows[i] : i;
+    const float* x = a.X + (size_t)src * a.ldx;
+    const float rs = row_rstd(x, a.d, a.eps, red);
+    for (int j = threadIdx.x; j < a.d; j += blockDim.x) hn[j] = x[j] * rs;
+    __syncthreads();
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int b0 = part * 64 + wave * 16;
+    const bf16_t* W = (const bf16_t*)a.W + (size_t)b0 * a.d + lane * 8;
+    float acc[16];
+#pragma unroll
+    for (int b = 0; b < 16; ++b) acc[b] = 0.f;
+    for (int c = 0; c < a.d; c += 512) {
+        uint4 w[16];
+#pragma unroll
+        for (int b = 0; b < 16; ++b) w[b] = *reinterpret_cast<const uint4*>(W + (size_t)b * a.d + c);
+        float h[8];
+        const float4 h0 = *reinterpret_cast<const float4*>(hn + c + lane * 8);
+        const float4 h1 = *reinterpret_cast<const float4*>(hn + c + lane * 8 + 4);
+        h[0] = h0.x; h[1] = h0.y; h[2] = h0.z; h[3] = h0.w; h[4] = h1.x; h[5] = h1.y; h[6] = h1.z; h[7] = h1.w;
+#pragma unroll
+        for (int b = 0; b < 16; ++b) {
+            float wf[8];
+            load8v<bf16_t>(reinterpret_cast<const bf16_t*>(&w[b]), wf);
+#pragma unroll
+            for (int u = 0; u < 8; ++u) acc[b] = fmaf(wf[u], h[u], acc[b]);
+        }
+    }
+    const __amdgpu_buffer_rsrc_t lgr = coherent_rsrc(a.lg + (size_t)i * a.n_bins);
+#pragma unroll
+    for (int b = 0; b < 16; ++b) {
+        const float v = wave_sum(acc[b]);
+        if (lane == b) st_coherent1(lgr, (b0 + b) * 4, v);
+    }
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+    if (threadIdx.x == 0)
+        s_last = __hip_atomic_fetch_add(a.counters + i, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
+                 (unsigned)(gridDim.y - 1);
+    __syncthreads();
+    if (!s_last || wave != 0) return;
+    float bv = -INFINITY;
+    int bi = 0x7fffffff;
+    for (int b = lane; b < a.n_bins; b += 64) {
+        const float v = ld_coherent1(lgr, b * 4);
+        if (v > bv || (v == bv && b < bi)) { bv = v; bi = b; }
+    }
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) {
+        const float ov = __shfl_xor(bv, off, 64);
+        const int oi = __shfl_xor(bi, off, 64);
+        if (ov > bv || (ov == bv && oi < bi)) { bv = ov; bi = oi; }
+    }
+    float sv = -INFINITY;
+    for (int b = lane; b < a.n_bins; b += 64)
+        if (b != bi) sv = fmaxf(sv, ld_coherent1(lgr, b * 4));
+    sv = wave_max(sv);
+    if (lane == 0) {
+        const int o = i * a.ntok + a.col;
+        a.tokens[o] = bi;
+        if (a.actions) a.actions[o] = -1.0f + (2.0f * (float)bi + 1.0f) / (float)a.n_bins;
+        if (a.margins) a.margins[o] = bv - sv;
+        __hip_atomic_store(a.counters + i, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+}
+
 void action_logits(const LogitsArgs& a, hipStream_t s) {
     if (a.n <= 0) return;
+    if (a.bf16 && a.lg && a.counters && a.d % 512 == 0 && a.n_bins % 64 == 0) {
+        hipLaunchKernelGGL(logits_split_kernel, dim3(a.n, a.n_bins / 64), dim3(256),
+                           (size_t)a.d * sizeof(float), s, a);
+        return;
+    }
     const size_t shm = (size_t)(a.d + a.n_bins) * sizeof(float);
     if (a.bf16) hipLaunchKernelGGL(logits_kernel<bf16_t>, dim3(a.n), dim3(256), shm, s, a);
     else hipLaunchKernelGGL(logits_kernel<float>, dim3(a.n), dim3(256), shm, s, a);
