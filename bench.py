@@ -35,6 +35,8 @@ WORKLOADS = {
     "flow-bf16": (4, 64, 1004),
     "ragged-7b": (3, 128, 1005),
 }
+# default oracle sample per workload: envs that take roughly 10-40 s on the host
+CPU_SAMPLE = {"tiny-fp32": 8, "small-bf16": 32, "7b-bf16": 1, "flow-bf16": 3, "ragged-7b": 0}
 PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA
 PEAK_FP32_TFLOPS = 157.3      # MI355X fp32 vector
 PEAK_HBM_GBS = 8000.0
@@ -42,6 +44,18 @@ PEAK_HBM_GBS = 8000.0
 
 def log(*a):
     print(*a, file=sys.stderr, flush=True)
+
+
+def stored_traffic(workload: str):
+    """Per-launch HBM traffic of the large-M GEMM measured with hardware
+    counters (pmc_traffic.py), if taken on the current GEMM sources."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{workload}.json")
+    if not os.path.exists(path):
+        return None
+    import pmc_traffic
+    with open(path) as f:
+        t = json.load(f)
+    return t if t.get("sources_sha") == pmc_traffic.sources_hash() else None
 
 
 def cpu_baseline(workload: str, n_sample: int):
@@ -159,7 +173,8 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="small-bf16", choices=sorted(WORKLOADS))
-    ap.add_argument("--cpu-sample", type=int, default=16, help="envs in the oracle sample (0 = skip)")
+    ap.add_argument("--cpu-sample", type=int, default=None,
+                    help="envs in the oracle sample (0 = skip; default: about 10-40 s of oracle work)")
     ap.add_argument("--partitions", action="store_true",
                     help="also time the steps on CU-masked streams of 25/50/75%% of the CUs")
     args = ap.parse_args()
@@ -265,18 +280,27 @@ def main():
         achieved = dom["bytes"] / (dom["ms"] * 1e6) if dom["ms"] else 0.0
         roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s"}
         per_launch = {"bytes_per_launch": round(dom["bytes"] / max(1, dom["launches"]))}
-    roofline.update({"frac": round(achieved / roofline["peak"], 4), "traffic": None,
+    traffic = stored_traffic(args.workload) if dominant == E.K_GEMM else None
+    roofline.update({"frac": round(achieved / roofline["peak"], 4),
+                     "traffic": traffic["traffic_bytes_per_launch"] if traffic else None,
                      "kernel": {E.K_GEMM: "gemm_bf16_big_kernel (projections, M >= 256)",
-                                E.K_GEMM_SKINNY: "gemm_bf16_kernel split-K + reduce (decode projections)",
+                                E.K_GEMM_SKINNY: "gemm_bf16_decode_kernel (decode projections, split-K reduced in-kernel)",
                                 E.K_ATTN_PREFILL: "attn_prefill_bf16_kernel",
-                                E.K_ATTN_DECODE: "attn_decode_split_kernel + combine",
+                                E.K_ATTN_DECODE: "attn_decode_bf16_kernel",
                                 E.K_OTHER: "row-wise kernels"}[dominant],
                      "launches": dom["launches"],
                      "avg_launch_us": round(1000 * dom["ms"] / max(1, dom["launches"]), 2),
                      "share_of_step": round(dom["ms"] / gpu_ms, 3) if gpu_ms else None})
     roofline.update(per_launch)
+    roofline["algorithmic_bytes_per_launch"] = round(dom["bytes"] / max(1, dom["launches"]))
+    if traffic:
+        roofline["traffic_unit"] = "bytes per launch: rocprofv3 FETCH_SIZE + WRITE_SIZE, scaled by a 1 GiB copy"
+        roofline["traffic_over_algorithmic"] = round(
+            traffic["traffic_bytes_per_launch"] / max(1, roofline["algorithmic_bytes_per_launch"]), 3)
 
     base = None
+    if args.cpu_sample is None:
+        args.cpu_sample = CPU_SAMPLE[args.workload]
     if args.cpu_sample > 0 and args.workload != "ragged-7b":
         log("timing the CPU oracle ...")
         base = cpu_baseline(args.workload, args.cpu_sample)
