@@ -179,8 +179,8 @@ def main():
                     help="also time the steps on CU-masked streams of 25/50/75%% of the CUs")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}); environments "
-              "are independent, so N GPUs would each run their own share (see DESIGN.md, sharding)",
+        print(f"bench.py: measures one GPU only (asked for --gpus {args.gpus}); environments are "
+              "independent, so N GPUs would each run their own share of them with replicated weights",
               file=sys.stderr)
         sys.exit(2)
 

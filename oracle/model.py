@@ -10,7 +10,7 @@ observation (camera frames plus a task instruction) and produces the next
 action (Section 2.1, "Embodied Models"; Section 2.2, generation stage): a
 vision-language backbone fuses the inputs into a KV cache that an action head
 consumes.  The paper fixes the family but no architecture, so the concrete
-policy below is a *reading* (listed in DESIGN.md, "Readings"):
+policy below is a *reading* of the paper (one choice among many it allows):
 
 * patchify + linear patch embedding; for the 7B-class model a 24-layer
   non-causal ViT with learned position embeddings and a projector;

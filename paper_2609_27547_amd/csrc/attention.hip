@@ -3,17 +3,21 @@
 // h / (q_heads / kv_heads).
 //
 // attn_prefill_bf16: flash attention for prefill, the ViT and the flow
-//   expert.  A workgroup (4 waves) owns 64 query rows of one head; each wave
+//   expert.  A workgroup (4 waves) owns 64 query rows of one head; 64-key K
+//   and V tiles are DMA'd from the paged cache into double-buffered LDS
+//   (whole 128/256-byte rows, XOR-swizzled 16-byte chunks).  Each wave
 //   computes S^T = K Q^T for its 16 queries with v_mfma_f32_16x16x32_bf16 so
 //   that every lane holds the scores of a single query, runs the online
 //   softmax in fp32 with exp2, and feeds the probabilities straight back as
-//   the B operand of O^T = V^T P^T (V staged transposed in LDS).  P enters
-//   the bf16 product as 2^(x - ceil(max x)), x = s log2(e) / sqrt(hd), with
-//   the row sum taken before rounding.
+//   the B operand of O^T = V^T P^T; V stays row-major in LDS and the
+//   transposed fragments come from ds_read_b64_tr_b16.  P enters the bf16
+//   product as 2^(x - ceil(max x)), x = s log2(e) / sqrt(hd), with the row
+//   sum taken before rounding.
 // attn_prefill_f32: plain per-(query, head) kernel for fp32 policies.
-// attn_decode: one query per sequence; keys split into 64-key chunks, each
-//   chunk a workgroup that streams its K and V rows once with 16-byte loads;
-//   a second kernel combines the chunks in chunk order.
+// attn_decode_bf16: one query per sequence; one workgroup per (sequence,
+//   head) streams the whole cache with whole-row loads and merges its four
+//   waves' partial softmax results in LDS.  attn_decode_split (+ combine):
+//   the fp32 path, 64-key chunks merged by a second kernel in chunk order.
 #include <math.h>
 
 #include "kernels.h"

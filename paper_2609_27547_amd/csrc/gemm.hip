@@ -1,15 +1,25 @@
 // Projections y = x W^T of every linear layer (W stored [out, in]).
 //
-// bf16 path: MFMA v_mfma_f32_16x16x32_bf16 tiles, LDS double buffer, fp32
-// accumulate.  The weight tile feeds the MFMA "A" operand and the activation
-// tile the "B" operand, so a lane ends up owning four consecutive output
-// columns of one row: epilogues write 8-16 contiguous bytes per lane and a
-// SwiGLU gate/up pair lands in the same lane (weights packed in 32-row
-// groups: 16 gate rows, then the 16 matching up rows).
+// bf16 path, three kernels, all on v_mfma_f32_16x16x32_bf16 with fp32
+// accumulation.  The weight tile feeds the MFMA "A" operand and the
+// activation tile the "B" operand, so a lane ends up owning four consecutive
+// output columns of one row: a SwiGLU gate/up pair lands in the same lane
+// (weights packed in 32-row groups: 16 gate rows, then the 16 matching up
+// rows), and so does a rotary pair of the fused QKV projection.
+//  * gemm_bf16_big_kernel (M >= 256: prefill, ViT, flow expert): 256 x 256
+//    tiles, 16 waves, operands DMA'd global -> LDS, epilogue staged through
+//    LDS for whole-row stores.
+//  * gemm_bf16_decode_kernel (decode, M <= 256): 64-column slices, per-wave
+//    LDS pipelines fed by whole-line DMA; K split across workgroups only for
+//    narrow outputs, the partials summed in split order inside the kernel by
+//    the last workgroup of each tile.
+//  * gemm_bf16_kernel: register-staged LDS tiles for the remaining shapes
+//    (K not a multiple of 64), with split-K partials reduced in split order
+//    by splitk_reduce_kernel.
 // fp32 path (fp32 policies): LDS-tiled FMA kernel with the same epilogues.
-// Split over K (decode-sized M): fp32 partials per split, then a reduction
-// that sums splits in a fixed order and applies the epilogue, so results do
-// not depend on timing or on the number of compute units.
+// Every tile and split choice is a function of (N, K) -- plus M >= 256 for
+// the large-M kernel -- so results do not depend on timing, on the number of
+// compute units or on how many rows a decode call holds.
 #include "kernels.h"
 
 namespace ebrl {

@@ -35,10 +35,16 @@ GEMM_SOURCES = ["paper_2609_27547_amd/csrc/gemm.hip", "paper_2609_27547_amd/csrc
 
 
 def sources_hash(paths=GEMM_SOURCES) -> str:
+    """Hash of the code (comments and blank lines dropped) of the sources."""
+    import re
     h = hashlib.sha256()
     for p in paths:
-        with open(os.path.join(ROOT, p), "rb") as f:
-            h.update(f.read())
+        with open(os.path.join(ROOT, p)) as f:
+            text = re.sub(r"/\*.*?\*/", "", f.read(), flags=re.S)
+        for line in text.splitlines():
+            line = re.sub(r"//.*", "", line).strip()
+            if line:
+                h.update(line.encode() + b"\n")
     return h.hexdigest()[:16]
 
 
