@@ -282,6 +282,23 @@ typedef __attribute__((address_space(3))) void* lds_ptr_t;
 
 EBRL_DEV void wait_vm_all() { __builtin_amdgcn_s_waitcnt(0); }
 
+// s_waitcnt on the vector-memory counter only (gfx9 encoding: expcnt and
+// lgkmcnt fields at their maxima).
+template <int N> EBRL_DEV void wait_vmcnt() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt((N & 15) | 0x70 | 0xF00 | ((N >> 4) << 14));
+}
+
+// global_load_lds_dwordx4 issued as inline assembly: the compiler neither
+// counts these loads nor guards LDS reads against them, so its own waits
+// stay partial; kernels that use it wait on vmcnt and synchronise
+// themselves before reading what the DMA filled.
+EBRL_DEV void dma16_to_lds(const void* g, uint32_t lds_addr) {
+    asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+                 :: "v"(g), "s"(lds_addr) : "memory", "m0");
+}
+
+
 template <int ROWS, int NW>
 EBRL_DEV void load_tile_lds(const bf16_t* __restrict__ G, int ld, int row0_g, int rows_valid, int k0,
                             bf16_t* lds_tile, int wave, int lane) {
@@ -301,12 +318,11 @@ EBRL_DEV bf16x8 lds_frag(const bf16_t* tile, int row, int c) {
     return *reinterpret_cast<const bf16x8*>(tile + row * 64 + ((c ^ (row & 7)) << 3));
 }
 
-template <int BN, int WM, int WN, bool PAIRED, bool SPLIT, class Epi>
-__global__ __launch_bounds__(64 * WM * WN, 1) void gemm_bf16_big_kernel(
+template <int BM, int BN, int WM, int WN, bool PAIRED, bool SPLIT, class Epi>
+__global__ __launch_bounds__(64 * WM * WN, WM * WN == 4 ? 2 : 1) void gemm_bf16_big_kernel(
     const bf16_t* __restrict__ A, int lda, const bf16_t* __restrict__ B, int ldb, int M, int N, int K,
     int k_per_split, float* __restrict__ ws, Epi epi)
 {
-    constexpr int BM = 256;
     constexpr int NW = WM * WN;
     constexpr int WTM = BM / WM, WTN = BN / WN;
     constexpr int TM = WTM / 16, TN = WTN / 16;
@@ -396,10 +412,14 @@ __global__ __launch_bounds__(64 * WM * WN, 1) void gemm_bf16_big_kernel(
     // 16-32-byte pieces of 16 rows.  Rows are padded to 68 floats so the
     // fragment-layout writes spread over the banks.
     static_assert(!SPLIT, "the large-M kernel never splits K");
-    static_assert(WTN == 64 && NW == 16, "staging assumes 64-column wave tiles, 16 waves");
+    static_assert(WTN == 64, "staging assumes 64-column wave tiles");
     constexpr int SROW = 68;
-    bf16_t* const region = wave < 4 ? sA0 : (wave < 8 ? sA1 : (wave < 12 ? sB0 : sB1));
-    float* const stage = reinterpret_cast<float*>(region) + (wave & 3) * 16 * SROW;
+    constexpr int PER_A = (BM * 64 * 2) / (16 * SROW * 4), PER_B = (BN * 64 * 2) / (16 * SROW * 4);
+    static_assert(2 * (PER_A + PER_B) >= NW, "staging space");
+    bf16_t* const region = wave < PER_A ? sA0 : (wave < 2 * PER_A ? sA1 : (wave < 2 * PER_A + PER_B ? sB0 : sB1));
+    const int slot = wave < PER_A ? wave : (wave < 2 * PER_A ? wave - PER_A
+                                            : (wave < 2 * PER_A + PER_B ? wave - 2 * PER_A : wave - 2 * PER_A - PER_B));
+    float* const stage = reinterpret_cast<float*>(region) + slot * 16 * SROW;
     const int ncol0 = n0 + wn * WTN;
 #pragma unroll
     for (int i = 0; i < TM; ++i) {
@@ -457,23 +477,10 @@ constexpr int DEC_MAX_SPLITS = 16;
 constexpr int DEC_TILE_FLOATS = 64 * 64;   // partial-tile stride in the workspace
 constexpr int DEC_MAX_COUNTERS = 4096;
 
-// s_waitcnt on the vector-memory counter only (gfx9 encoding: expcnt and
-// lgkmcnt fields at their maxima).
-template <int N> EBRL_DEV void wait_vmcnt() {
-    static_assert(N >= 0 && N < 64, "vmcnt range");
-    __builtin_amdgcn_s_waitcnt((N & 15) | 0x70 | 0xF00 | ((N >> 4) << 14));
-}
-
 // One wave's DMA of ROWS rows x 64 bf16 (K group k0) into `lds`: row q of the
 // group sits in instruction q / 8, lane (q % 8) * 8 + (c ^ (q % 8)) holds its
-// 16-byte chunk c (the XOR spreads a fragment read over the banks).  Issued
-// as inline assembly, so the compiler neither counts these loads nor guards
-// LDS reads against them: the caller waits on vmcnt itself (each wave reads
-// only the region its own DMA fills).
-EBRL_DEV void dma16_to_lds(const void* g, uint32_t lds_addr) {
-    asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
-                 :: "v"(g), "s"(lds_addr) : "memory", "m0");
-}
+// 16-byte chunk c (the XOR spreads a fragment read over the banks).  Each
+// wave reads only the region its own DMA fills.
 template <int ROWS>
 EBRL_DEV void dec_dma(const bf16_t* __restrict__ G, int ld, int row0, int rows_valid, int k0, bf16_t* lds,
                       int lane) {
@@ -873,9 +880,19 @@ template <bool PAIRED, class Epi>
 static void launch_bf16(const GemmArgs& a, const GemmPlan& p, Epi epi, hipStream_t s) {
     const bool split = p.splits > 1;
     if (p.big) {
-        dim3 grid(((a.M + 255) / 256) * ((a.N + 255) / 256), 1);
-        hipLaunchKernelGGL((gemm_bf16_big_kernel<256, 4, 4, PAIRED, false, Epi>), grid, dim3(1024), 0, s,
-                           (const bf16_t*)a.A, a.lda, (const bf16_t*)a.B, a.ldb, a.M, a.N, a.K, a.K, a.ws, epi);
+        // 256 x 256 tiles, or 128 x 128 (4 waves, two workgroups per CU)
+        // when the large tiles would fill less than half the chip; the K
+        // order of every sum is the same either way
+        const long t256 = (long)((a.M + 255) / 256) * ((a.N + 255) / 256);
+        if (t256 >= 128) {
+            dim3 grid((unsigned)t256, 1);
+            hipLaunchKernelGGL((gemm_bf16_big_kernel<256, 256, 4, 4, PAIRED, false, Epi>), grid, dim3(1024), 0, s,
+                               (const bf16_t*)a.A, a.lda, (const bf16_t*)a.B, a.ldb, a.M, a.N, a.K, a.K, a.ws, epi);
+        } else {
+            dim3 grid(((a.M + 127) / 128) * ((a.N + 127) / 128), 1);
+            hipLaunchKernelGGL((gemm_bf16_big_kernel<128, 128, 2, 2, PAIRED, false, Epi>), grid, dim3(256), 0, s,
+                               (const bf16_t*)a.A, a.lda, (const bf16_t*)a.B, a.ldb, a.M, a.N, a.K, a.K, a.ws, epi);
+        }
         return;
     }
     if (p.dec) {
