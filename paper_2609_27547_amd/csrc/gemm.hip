@@ -825,14 +825,14 @@ static GemmPlan plan_gemm(bool bf16, int M, int N, int K, size_t ws_floats, bool
     p.splits = 1;
     p.k_per_split = K;
     if (bf16 && split_ok && K % 64 == 0) {
-        // About 128 workgroups from column slices x K splits, a split at
-        // least 16 K groups (1024 wide): the cross-workgroup hand-off costs
-        // about as much as streaming that much more per workgroup.  The
-        // partial tiles of up to four row tiles must fit the workspace.
+        // K splits: about 64 (column slice, split) pairs, each split at least
+        // 16 K groups (1024 wide) -- the cross-workgroup hand-off costs about
+        // as much as streaming that much more.  A function of (N, K) only.
+        // The partial tiles of up to four row tiles must fit the workspace.
         p.dec = true;
         const int tiles_n = (N + DEC_BN - 1) / DEC_BN;
         const int kgroups = K / 64;
-        const int want = std::max(1, std::min({(128 + tiles_n - 1) / tiles_n, kgroups / 16, DEC_MAX_SPLITS}));
+        const int want = std::max(1, std::min({(64 + tiles_n - 1) / tiles_n, kgroups / 16, DEC_MAX_SPLITS}));
         int gps = (kgroups + want - 1) / want;
         for (;;) {
             const int sp = (kgroups + gps - 1) / gps;
@@ -844,7 +844,12 @@ static GemmPlan plan_gemm(bool bf16, int M, int N, int K, size_t ws_floats, bool
         }
         p.steps_per_split = gps;
         p.splits = (kgroups + gps - 1) / gps;
-        p.tm = M <= 16 ? 1 : (M <= 32 ? 2 : 4);
+        // Row tiles of 16, 32 or 64 rows (any choice leaves every sum's
+        // order unchanged): up to four row tiles when the column slices x
+        // splits alone fill under half the chip -- each workgroup then
+        // streams a quarter of the activations; otherwise the fewest tiles.
+        if ((long)tiles_n * p.splits >= 128) p.tm = M <= 16 ? 1 : (M <= 32 ? 2 : 4);
+        else p.tm = M <= 64 ? 1 : (M <= 128 ? 2 : 4);
         p.m_tiles = (M + 16 * p.tm - 1) / (16 * p.tm);
         return p;
     }
