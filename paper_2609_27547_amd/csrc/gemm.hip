@@ -472,7 +472,7 @@ __global__ __launch_bounds__(64 * WM * WN, WM * WN == 4 ? 2 : 1) void gemm_bf16_
 // workgroup that finishes a tile last (a device-scope counter per tile) sums
 // the partials in split order, runs the epilogue and clears the counter for
 // the next call.  An element's summation order depends only on (N, K).
-constexpr int DEC_BN = 64;
+constexpr int DEC_BN = 64;   // column slice of the split rule (the kernel also runs 32-wide slices)
 constexpr int DEC_MAX_SPLITS = 16;
 constexpr int DEC_TILE_FLOATS = 64 * 64;   // partial-tile stride in the workspace
 constexpr int DEC_MAX_COUNTERS = 4096;
@@ -496,17 +496,18 @@ EBRL_DEV bf16x8 dec_frag(const bf16_t* lds, int row, int c) {
     return *reinterpret_cast<const bf16x8*>(lds + (row >> 3) * 512 + ((row & 7) * 8 + (c ^ (row & 7))) * 8);
 }
 
-template <int TM, bool PAIRED, class Epi>
+template <int TM, int BN, bool PAIRED, class Epi>
 __global__ __launch_bounds__(256) void gemm_bf16_decode_kernel(
     const bf16_t* __restrict__ A, int lda, const bf16_t* __restrict__ W, int ldw, int M, int N,
     int K, int groups_per_split, int splits, int m_tiles, float* __restrict__ ws,
     unsigned* __restrict__ counters, Epi epi)
 {
-    constexpr int TN = DEC_BN / 16;
+    constexpr int TN = BN / 16;
+    static_assert(!PAIRED || TN % 2 == 0, "paired epilogue needs fragment pairs");
     constexpr int FR = TM * TN;            // output fragments per wave
-    constexpr int WE = DEC_BN * 64;        // bf16 per wave per buffer: weights
+    constexpr int WE = BN * 64;            // bf16 per wave per buffer: weights
     constexpr int XE = TM * 16 * 64;       //                             activations
-    constexpr int NDMA = (DEC_BN + TM * 16) / 8;   // DMA instructions per K group
+    constexpr int NDMA = (BN + TM * 16) / 8;       // DMA instructions per K group
     // one __shared__ object per buffer and operand, so that the compiler can
     // tell the buffer being read from the one the DMA is filling
     __shared__ __attribute__((aligned(1024))) bf16_t sW0[4 * WE];
@@ -519,7 +520,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_decode_kernel(
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int r = lane & 15, g = lane >> 4;
-    const int tiles_n = (N + DEC_BN - 1) / DEC_BN;
+    const int tiles_n = (N + BN - 1) / BN;
     // XCD-aware order: the row tiles of one (column slice, split) pair --
     // which read the same weights -- run on the same XCD.
     int bid = blockIdx.x;
@@ -528,7 +529,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_decode_kernel(
     const int mt = bid % m_tiles;
     const int unit = bid / m_tiles;
     const int split = unit % splits, nt = unit / splits;
-    const int m0 = mt * 16 * TM, n0 = nt * DEC_BN;
+    const int m0 = mt * 16 * TM, n0 = nt * BN;
     const int kgroups = K >> 6;
     const int s_begin = split * groups_per_split;
     const int s_end = min(kgroups, s_begin + groups_per_split);
@@ -539,7 +540,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_decode_kernel(
     bf16_t* const w0 = sW0 + wave * WE; bf16_t* const x0 = sX0 + wave * XE;
     bf16_t* const w1 = sW1 + wave * WE; bf16_t* const x1 = sX1 + wave * XE;
     auto dma = [&](int grp, bf16_t* wl, bf16_t* xl) {
-        dec_dma<DEC_BN>(W, ldw, n0, N, grp * 64, wl, lane);
+        dec_dma<BN>(W, ldw, n0, N, grp * 64, wl, lane);
         dec_dma<TM * 16>(A, lda, m0, M, grp * 64, xl, lane);
     };
 
@@ -810,7 +811,7 @@ __global__ void splitk_reduce_kernel(const float* __restrict__ ws, int splits, i
 // Tile and split choice depend only on (M, N, K).
 struct GemmPlan {
     int bm; int bn; int splits; int k_per_split; bool big;
-    bool dec; int steps_per_split; int tm; int m_tiles;   // decode kernel (steps: 64-wide K groups)
+    bool dec; int steps_per_split; int tm; int m_tiles; int dbn;   // decode kernel (steps: 64-wide K groups)
 };
 
 // Kernel and split choice.  The tile variant never changes an element's
@@ -828,7 +829,8 @@ static GemmPlan plan_gemm(bool bf16, int M, int N, int K, size_t ws_floats, bool
         // K splits: about 64 (column slice, split) pairs, each split at least
         // 16 K groups (1024 wide) -- the cross-workgroup hand-off costs about
         // as much as streaming that much more.  A function of (N, K) only.
-        // The partial tiles of up to four row tiles must fit the workspace.
+        // The partial tiles (up to four row tiles, 32- or 64-column slices:
+        // at most 8 x tiles_n tiles) must fit the workspace and counters.
         p.dec = true;
         const int tiles_n = (N + DEC_BN - 1) / DEC_BN;
         const int kgroups = K / 64;
@@ -837,8 +839,8 @@ static GemmPlan plan_gemm(bool bf16, int M, int N, int K, size_t ws_floats, bool
         for (;;) {
             const int sp = (kgroups + gps - 1) / gps;
             if (sp == 1) break;
-            if (sp <= DEC_MAX_SPLITS && (size_t)sp * 4 * tiles_n * DEC_TILE_FLOATS <= ws_floats &&
-                4 * tiles_n <= DEC_MAX_COUNTERS)
+            if (sp <= DEC_MAX_SPLITS && (size_t)sp * 8 * tiles_n * DEC_TILE_FLOATS <= ws_floats &&
+                8 * tiles_n <= DEC_MAX_COUNTERS)
                 break;
             ++gps;
         }
@@ -851,6 +853,8 @@ static GemmPlan plan_gemm(bool bf16, int M, int N, int K, size_t ws_floats, bool
         if ((long)tiles_n * p.splits >= 128) p.tm = M <= 16 ? 1 : (M <= 32 ? 2 : 4);
         else p.tm = M <= 64 ? 1 : (M <= 128 ? 2 : 4);
         p.m_tiles = (M + 16 * p.tm - 1) / (16 * p.tm);
+        // 32-column slices when that still leaves under 3/4 of the chip idle
+        p.dbn = (long)tiles_n * p.splits * p.m_tiles < 192 ? 32 : 64;
         return p;
     }
     if (bf16 && !split_ok && M >= 256 && K % 64 == 0) {
@@ -901,16 +905,21 @@ static void launch_bf16(const GemmArgs& a, const GemmPlan& p, Epi epi, hipStream
         return;
     }
     if (p.dec) {
-        const int tiles_n = (a.N + DEC_BN - 1) / DEC_BN;
-        dim3 grid(tiles_n * p.splits * p.m_tiles);
-        auto godec = [&](auto kern) {
+        auto godec = [&](auto kern, int bn) {
+            dim3 grid(((a.N + bn - 1) / bn) * p.splits * p.m_tiles);
             hipLaunchKernelGGL(kern, grid, dim3(256), 0, s, (const bf16_t*)a.A, a.lda, (const bf16_t*)a.B,
                                a.ldb, a.M, a.N, a.K, p.steps_per_split, p.splits, p.m_tiles, a.ws,
                                a.counters, epi);
         };
-        if (p.tm == 1) godec(gemm_bf16_decode_kernel<1, PAIRED, Epi>);
-        else if (p.tm == 2) godec(gemm_bf16_decode_kernel<2, PAIRED, Epi>);
-        else godec(gemm_bf16_decode_kernel<4, PAIRED, Epi>);
+        if (p.dbn == 32) {
+            if (p.tm == 1) godec(gemm_bf16_decode_kernel<1, 32, PAIRED, Epi>, 32);
+            else if (p.tm == 2) godec(gemm_bf16_decode_kernel<2, 32, PAIRED, Epi>, 32);
+            else godec(gemm_bf16_decode_kernel<4, 32, PAIRED, Epi>, 32);
+        } else {
+            if (p.tm == 1) godec(gemm_bf16_decode_kernel<1, 64, PAIRED, Epi>, 64);
+            else if (p.tm == 2) godec(gemm_bf16_decode_kernel<2, 64, PAIRED, Epi>, 64);
+            else godec(gemm_bf16_decode_kernel<4, 64, PAIRED, Epi>, 64);
+        }
         return;
     }
     auto go = [&](auto kern, int bm, int bn) {
