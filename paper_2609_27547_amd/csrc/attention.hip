@@ -144,7 +144,7 @@ __global__ __launch_bounds__(256) void attn_prefill_bf16_kernel(AttnPrefillArgs 
                 s[kt][v] = val;
                 tmax = fmaxf(tmax, val);
             }
-        tmax = fmaxf(tmax, __shfl_xor(tmax, 16, 64));
+        tmax = fmaxf(tmax, swz_xor16_f(tmax));
         tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
         // The running maximum is kept as an integer (ceil, in log2 units):
         // rescaling by alpha is then a power of two, which commutes with the
@@ -162,7 +162,7 @@ __global__ __launch_bounds__(256) void attn_prefill_bf16_kernel(AttnPrefillArgs 
                 s[kt][v] = p;
                 psum += p;
             }
-        psum += __shfl_xor(psum, 16, 64);
+        psum += swz_xor16_f(psum);
         psum += __shfl_xor(psum, 32, 64);
         l_i = l_i * alpha + psum;
         m_i = m_new;
@@ -448,8 +448,7 @@ __global__ __launch_bounds__(256) void attn_decode_bf16_kernel(AttnDecodeArgs a,
             float dot = 0.f;
 #pragma unroll
             for (int j = 0; j < 8; ++j) dot = fmaf(q[j], kv[j], dot);
-#pragma unroll
-            for (int off = LPK / 2; off > 0; off >>= 1) dot += __shfl_xor(dot, off, 64);
+            dot = LPK == 8 ? sum_lanes8(dot) : sum_lanes16(dot);
             sc[t] = (kb + t * KPL + kq < we) ? dot * scale_log2 : -INFINITY;
             mr = fmaxf(mr, sc[t]);
         }
@@ -471,12 +470,14 @@ __global__ __launch_bounds__(256) void attn_decode_bf16_kernel(AttnDecodeArgs a,
         m_run = m_new;
     }
     // lanes of one key slot hold the same l; sum over the key slots
+    auto slots_sum = [&](float v) {
+        if (LPK == 8) v += dpp_f<DPP_ROR8>(v);
+        v += swz_xor16_f(v);
+        return v + __shfl_xor(v, 32, 64);
+    };
+    l_run = slots_sum(l_run);
 #pragma unroll
-    for (int off = LPK; off < 64; off <<= 1) {
-        l_run += __shfl_xor(l_run, off, 64);
-#pragma unroll
-        for (int j = 0; j < 8; ++j) acc[j] += __shfl_xor(acc[j], off, 64);
-    }
+    for (int j = 0; j < 8; ++j) acc[j] = slots_sum(acc[j]);
     if (kq == 0) {
 #pragma unroll
         for (int j = 0; j < 8; ++j) s_o[wave][sub * 8 + j] = acc[j];

@@ -40,16 +40,48 @@ template <> EBRL_DEV void st4<bf16_t>(bf16_t* p, float a, float b, float c, floa
     *reinterpret_cast<uint2*>(p) = u;
 }
 
-EBRL_DEV float wave_sum(float v) {
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
-    return v;
+// Cross-lane reductions without LDS round trips where possible: DPP
+// quad_perm / row_half_mirror / row_mirror / row_ror inside 16-lane rows,
+// ds_swizzle (xor 16 inside 32 lanes) across rows, v_readlane across the two
+// wave halves.  Float add and max are commutative, so the two lanes of every
+// exchange compute the same value and a reduction leaves every lane of its
+// group with the identical result.
+template <int CTRL> EBRL_DEV float dpp_f(float v) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL, 0xF, 0xF, false));
 }
-
+constexpr int DPP_SWAP1 = 0xB1;        // quad_perm [1, 0, 3, 2]
+constexpr int DPP_SWAP2 = 0x4E;        // quad_perm [2, 3, 0, 1]
+constexpr int DPP_HALF_MIRROR = 0x141; // lane i <-> 7 - i within 8
+constexpr int DPP_MIRROR = 0x140;      // lane i <-> 15 - i within 16
+constexpr int DPP_ROR8 = 0x128;        // lane i <- lane (i + 8) % 16 within 16
+EBRL_DEV float swz_xor16_f(float v) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_ds_swizzle(__builtin_bit_cast(int, v), 0x401F));
+}
+// sum over each aligned group of 8 / 16 lanes
+EBRL_DEV float sum_lanes8(float v) {
+    v += dpp_f<DPP_SWAP1>(v);
+    v += dpp_f<DPP_SWAP2>(v);
+    return v + dpp_f<DPP_HALF_MIRROR>(v);
+}
+EBRL_DEV float sum_lanes16(float v) { v = sum_lanes8(v); return v + dpp_f<DPP_MIRROR>(v); }
+EBRL_DEV float max_lanes16(float v) {
+    v = fmaxf(v, dpp_f<DPP_SWAP1>(v));
+    v = fmaxf(v, dpp_f<DPP_SWAP2>(v));
+    v = fmaxf(v, dpp_f<DPP_HALF_MIRROR>(v));
+    return fmaxf(v, dpp_f<DPP_MIRROR>(v));
+}
+EBRL_DEV float readlane_f(float v, int l) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), l));
+}
+EBRL_DEV float wave_sum(float v) {
+    v = sum_lanes16(v);
+    v += swz_xor16_f(v);
+    return readlane_f(v, 0) + readlane_f(v, 32);
+}
 EBRL_DEV float wave_max(float v) {
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) v = fmaxf(v, __shfl_xor(v, off, 64));
-    return v;
+    v = max_lanes16(v);
+    v = fmaxf(v, swz_xor16_f(v));
+    return fmaxf(readlane_f(v, 0), readlane_f(v, 32));
 }
 
 // Block-wide sum over blockDim.x threads (multiple of 64, <= 1024); every
