@@ -197,40 +197,48 @@ void embed_rows(bool bf16, const void* E, int n_rows_e, int d, const int* ids, c
 }
 
 // ----------------------------------------------------------- patchify --
+// One thread per 8 consecutive K elements of a patch row (a 16-byte bf16
+// store); 32-bit index arithmetic.  kpad % 8 == 0; K elements past P*P*3 are
+// the zero padding.
 template <typename T>
-__global__ void im2col_kernel(const float* img, long total, int cams, int H, int W, int P, T* out,
-                              int kpad)
+__global__ __launch_bounds__(256) void im2col_kernel(const float* img, int rows, int cams, int H, int W, int P,
+                                                     T* out, int kpad)
 {
     const int gw = W / P, np = (H / P) * gw;
-    const int kreal = P * P * 3;
-    for (long e = blockIdx.x * (long)blockDim.x + threadIdx.x; e < total;
-         e += (long)gridDim.x * blockDim.x) {
-        const long row = e / kpad;
-        const int k = (int)(e - row * kpad);
-        float v = 0.f;
+    const int kreal = P * P * 3, kc = kpad / 8;
+    const int e = blockIdx.x * blockDim.x + threadIdx.x;
+    if (e >= rows * kc) return;
+    const int row = e / kc, k0 = (e - row * kc) * 8;
+    const int env = row / (cams * np), p = row - env * cams * np;
+    const int cam = p / np, pp = p - cam * np;
+    const int py = pp / gw, px = pp - py * gw;
+    const float* base = img + ((size_t)(env * cams + cam) * H + py * P) * W * 3 + (size_t)px * P * 3;
+    float v[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        const int k = k0 + j;
+        v[j] = 0.f;
         if (k < kreal) {
-            const int dy = k / (3 * P), rem = k - dy * 3 * P, dx = rem / 3, c = rem - dx * 3;
-            const long env = row / ((long)cams * np);
-            const int p = (int)(row - env * cams * np);
-            const int cam = p / np, pp = p - cam * np;
-            const int py = pp / gw, px = pp - py * gw;
-            v = img[((((env * cams + cam) * H) + py * P + dy) * (long)W + px * P + dx) * 3 + c];
+            const int dy = k / (3 * P), rem = k - dy * 3 * P;
+            v[j] = base[(size_t)dy * W * 3 + rem];
         }
-        st_elem<T>(out + e, v);
     }
+    st4<T>(out + (size_t)e * 8, v[0], v[1], v[2], v[3]);
+    st4<T>(out + (size_t)e * 8 + 4, v[4], v[5], v[6], v[7]);
 }
 
 void im2col(bool bf16, const float* img, int n, int cams, int H, int W, int P, void* out, int kpad,
             hipStream_t s) {
-    const long total = (long)n * cams * (H / P) * (W / P) * kpad;
-    if (total <= 0) return;
-    const int blocks = (int)std::min<long>((total + 255) / 256, 65536);
+    const long rows = (long)n * cams * (H / P) * (W / P);
+    if (rows <= 0) return;
+    const long threads = rows * (kpad / 8);
+    const int blocks = (int)((threads + 255) / 256);
     if (bf16)
-        hipLaunchKernelGGL(im2col_kernel<bf16_t>, dim3(blocks), dim3(256), 0, s, img, total, cams, H,
-                           W, P, (bf16_t*)out, kpad);
+        hipLaunchKernelGGL(im2col_kernel<bf16_t>, dim3(blocks), dim3(256), 0, s, img, (int)rows, cams, H, W, P,
+                           (bf16_t*)out, kpad);
     else
-        hipLaunchKernelGGL(im2col_kernel<float>, dim3(blocks), dim3(256), 0, s, img, total, cams, H,
-                           W, P, (float*)out, kpad);
+        hipLaunchKernelGGL(im2col_kernel<float>, dim3(blocks), dim3(256), 0, s, img, (int)rows, cams, H, W, P,
+                           (float*)out, kpad);
 }
 
 // --------------------------------------------------------- action head --
