@@ -64,6 +64,9 @@ __global__ __launch_bounds__(256) void attn_prefill_bf16_kernel(AttnPrefillArgs 
 
     int kv_end = kvlen;
     if (a.causal) kv_end = min(kvlen, qpos0 + min(qt0 + 64, qlen));
+    // first key that some lane of this wave must mask: the end of the keys, or
+    // (causal) the position of the wave's first query plus one
+    const int mask_from = a.causal ? min(kvlen, qpos0 + qt0 + wave * 16 + 1) : kvlen;
     const int ntiles = (kv_end + KT - 1) / KT;
     for (int b2 = tid; b2 < (kv_end + KV_BLOCK - 1) / KV_BLOCK; b2 += 256)
         s_bt[b2] = a.kv.block_table[(size_t)env * a.kv.bt_stride + b2];
@@ -134,16 +137,27 @@ __global__ __launch_bounds__(256) void attn_prefill_bf16_kernel(AttnPrefillArgs 
             }
         }
         float tmax = -INFINITY;
+        if (mask_from <= k0 + KT - 1) {
+            // tile reaches past the keys or past a query of this wave
 #pragma unroll
-        for (int kt = 0; kt < 4; ++kt)
+            for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
-            for (int v = 0; v < 4; ++v) {
-                const int kidx = k0 + kt * 16 + 4 * g + v;
-                const bool ok = kidx < kvlen && (!a.causal || kidx <= qpos);
-                const float val = ok ? s[kt][v] * scale_log2 : -INFINITY;
-                s[kt][v] = val;
-                tmax = fmaxf(tmax, val);
-            }
+                for (int v = 0; v < 4; ++v) {
+                    const int kidx = k0 + kt * 16 + 4 * g + v;
+                    const bool ok = kidx < kvlen && (!a.causal || kidx <= qpos);
+                    const float val = ok ? s[kt][v] * scale_log2 : -INFINITY;
+                    s[kt][v] = val;
+                    tmax = fmaxf(tmax, val);
+                }
+        } else {
+#pragma unroll
+            for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+                for (int v = 0; v < 4; ++v) {
+                    s[kt][v] *= scale_log2;
+                    tmax = fmaxf(tmax, s[kt][v]);
+                }
+        }
         tmax = fmaxf(tmax, swz_xor16_f(tmax));
         tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
         // The running maximum is kept as an integer (ceil, in log2 units):
@@ -166,8 +180,13 @@ __global__ __launch_bounds__(256) void attn_prefill_bf16_kernel(AttnPrefillArgs 
         psum += __shfl_xor(psum, 32, 64);
         l_i = l_i * alpha + psum;
         m_i = m_new;
+        // alpha is a power of two that is 1 once the integer running maximum
+        // stops growing: skip the rescale (exact either way) when it is 1 in
+        // every lane
+        if (__any(alpha != 1.0f)) {
 #pragma unroll
-        for (int i = 0; i < HD / 16; ++i) acc[i] *= alpha;
+            for (int i = 0; i < HD / 16; ++i) acc[i] *= alpha;
+        }
 
         // O^T += V^T P^T.  V stays row-major in LDS; ds_read_b64_tr_b16 hands
         // lane (r, g) the values of dimension 16 dt + r for 4 keys per read
