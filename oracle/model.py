@@ -403,15 +403,27 @@ class Policy:
         return {s: self.W(f"{kind}.{l}.{s}") for s in SLOT}
 
     # blocks ----------------------------------------------------------------
+    def _prenorm(self, x, folded):
+        """Operand of the projection after a pre-norm, and the row factor its
+        output is multiplied by.  Without bf16 emulation this is RMSNorm then
+        the product, exactly.  Emulating the bf16 policy's decode steps
+        (``folded``), the operand is the residual row rounded to bf16 and the
+        RMSNorm factor of that rounded row scales the product's rows;
+        otherwise the normalised row is rounded."""
+        if self.emulate_bf16 and folded:
+            h = self._r(x)
+            return h, 1.0 / np.sqrt(np.mean(h * h, axis=-1, keepdims=True) + self.cfg.eps)
+        return self._r(rmsnorm(x, self.cfg.eps)), 1.0
+
     def block(self, x, Wl, n_heads, n_kv, hd, pos, past_k=None, past_v=None, past_pos=None,
-              causal=True, use_rope=True):
+              causal=True, use_rope=True, folded=False):
         """Pre-norm transformer block.  Returns (x_out, k_new, v_new)."""
         t = x.shape[0]
         R = self._r
-        h = R(rmsnorm(x, self.cfg.eps))
-        q = linear(h, Wl["q"]).reshape(t, n_heads, hd)
-        k = linear(h, Wl["k"]).reshape(t, n_kv, hd)
-        v = linear(h, Wl["v"]).reshape(t, n_kv, hd)
+        h, f = self._prenorm(x, folded)
+        q = (linear(h, Wl["q"]) * f).reshape(t, n_heads, hd)
+        k = (linear(h, Wl["k"]) * f).reshape(t, n_kv, hd)
+        v = (linear(h, Wl["v"]) * f).reshape(t, n_kv, hd)
         if use_rope:
             q = rope(q, pos, self.cfg.rope_base)
             k = rope(k, pos, self.cfg.rope_base)
@@ -428,8 +440,8 @@ class Policy:
             o = multihead_attention(q, K, V, pos, kpos, causal)
         o = R(o.reshape(t, n_heads * hd))
         x = x + linear(o, Wl["o"])
-        h = R(rmsnorm(x, self.cfg.eps))
-        x = x + linear(R(silu(linear(h, Wl["gate"])) * linear(h, Wl["up"])), Wl["down"])
+        h, f = self._prenorm(x, folded)
+        x = x + linear(R(silu(linear(h, Wl["gate"]) * f) * (linear(h, Wl["up"]) * f)), Wl["down"])
         return x, k, v
 
     def _r(self, a):
@@ -547,7 +559,7 @@ class Policy:
             pos = np.array([st.T + step - 1])
             for l in range(cfg.layers):
                 x, k, v = self.block(x, self.layer("dec", l), cfg.q_heads, cfg.kv_heads,
-                                     cfg.head_dim, pos, ks[l], vs[l], kpos)
+                                     cfg.head_dim, pos, ks[l], vs[l], kpos, folded=True)
                 ks[l] = np.concatenate([ks[l], k], axis=0)
                 vs[l] = np.concatenate([vs[l], v], axis=0)
             kpos = np.concatenate([kpos, pos])

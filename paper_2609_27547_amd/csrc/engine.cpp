@@ -471,12 +471,25 @@ struct BlockCall {
     AttnDecodeArgs dec;
 };
 
+// Decode steps of bf16 policies fold each pre-norm into the projection that
+// follows it: the residual stream's producers (embedding, O and down
+// projections) also store the rows in bf16, and the QKV and gate/up decode
+// GEMMs scale their output rows by the RMSNorm factor of those rows.
+bool fold_decode_norm(const ebrl_policy* p, const StackDims& s, int rows) {
+    const int qkvn = (s.hq + 2 * s.hkv) * s.hd;
+    return p->bf16 && gemm_row_norm_ok(true, rows, qkvn, s.d, p->ws_floats) &&
+           gemm_row_norm_ok(true, rows, 2 * s.mlp, s.d, p->ws_floats);
+}
+
 int run_block(ebrl_policy* p, BlockCall& b) {
     const StackDims& s = *b.sd;
     const int qn = s.hq * s.hd, qkvn = (s.hq + 2 * s.hkv) * s.hd;
-    prof_begin(p, EBRL_K_OTHER);
-    rmsnorm_rows(p->bf16, b.R, s.d, nullptr, p->Xn, s.d, b.rows, s.d, 1e-6f, p->stream);
-    prof_end(p, 0, (double)b.rows * s.d * (4 + p->esz));
+    const bool fold = b.decode && fold_decode_norm(p, s, b.rows);
+    if (!fold) {
+        prof_begin(p, EBRL_K_OTHER);
+        rmsnorm_rows(p->bf16, b.R, s.d, nullptr, p->Xn, s.d, b.rows, s.d, 1e-6f, p->stream);
+        prof_end(p, 0, (double)b.rows * s.d * (4 + p->esz));
+    }
     // fused QKV projection: rotary embedding of Q and K and the paged K/V
     // write happen in the GEMM epilogue
     RopeKVArgs r;
@@ -485,7 +498,7 @@ int run_block(ebrl_policy* p, BlockCall& b) {
     r.row_pos = b.row_pos; r.cos_tab = p->cos_tab; r.sin_tab = p->sin_tab; r.use_rope = b.use_rope;
     GemmArgs g;
     g.A = p->Xn; g.lda = s.d; g.B = b.w->qkv; g.ldb = s.d; g.M = b.rows; g.N = qkvn; g.K = s.d;
-    g.epi = EPI_QKV; g.rope = &r;
+    g.epi = EPI_QKV; g.rope = &r; g.row_norm = fold;
     run_gemm(p, g, b.decode);
     if (b.decode) {
         b.dec.bf16 = p->bf16; b.dec.Q = p->Qb; b.dec.ldq = qn; b.dec.O = p->Ob; b.dec.ldo = qn;
@@ -503,17 +516,21 @@ int run_block(ebrl_policy* p, BlockCall& b) {
     g = GemmArgs();
     g.A = p->Ob; g.lda = qn; g.B = b.w->o; g.ldb = qn; g.M = b.rows; g.N = s.d; g.K = qn;
     g.epi = EPI_RESID; g.C = b.R; g.ldc = s.d;
+    if (fold) { g.xb = p->Xn; g.ldxb = s.d; }
     run_gemm(p, g, b.decode);
-    prof_begin(p, EBRL_K_OTHER);
-    rmsnorm_rows(p->bf16, b.R, s.d, nullptr, p->Xn, s.d, b.rows, s.d, 1e-6f, p->stream);
-    prof_end(p, 0, (double)b.rows * s.d * (4 + p->esz));
+    if (!fold) {
+        prof_begin(p, EBRL_K_OTHER);
+        rmsnorm_rows(p->bf16, b.R, s.d, nullptr, p->Xn, s.d, b.rows, s.d, 1e-6f, p->stream);
+        prof_end(p, 0, (double)b.rows * s.d * (4 + p->esz));
+    }
     g = GemmArgs();
     g.A = p->Xn; g.lda = s.d; g.B = b.w->gu; g.ldb = s.d; g.M = b.rows; g.N = 2 * s.mlp; g.K = s.d;
-    g.epi = EPI_SWIGLU; g.C = p->Hb; g.ldc = s.mlp;
+    g.epi = EPI_SWIGLU; g.C = p->Hb; g.ldc = s.mlp; g.row_norm = fold;
     run_gemm(p, g, b.decode);
     g = GemmArgs();
     g.A = p->Hb; g.lda = s.mlp; g.B = b.w->down; g.ldb = s.mlp; g.M = b.rows; g.N = s.d; g.K = s.mlp;
     g.epi = EPI_RESID; g.C = b.R; g.ldc = s.d;
+    if (fold) { g.xb = p->Xn; g.ldxb = s.d; }
     run_gemm(p, g, b.decode);
     return EBRL_OK;
 }
@@ -1065,6 +1082,7 @@ int ebrl_decode_actions(ebrl_policy* p, const int32_t* env_ids, int32_t n, int32
     if ((rc = upload_meta(p, m, false, &md))) return rc;
     const int max_splits = (maxT + steps + ATTN_DEC_CHUNK - 1) / ATTN_DEC_CHUNK;
 
+    const bool fold = fold_decode_norm(p, p->dec, n);
     auto body = [&]() -> int {
         LogitsArgs la;
         la.bf16 = p->bf16; la.W = p->w_act; la.d = c.d; la.n_bins = c.n_bins; la.n = n;
@@ -1077,7 +1095,7 @@ int ebrl_decode_actions(ebrl_policy* p, const int32_t* env_ids, int32_t n, int32
         for (int k = 1; k <= steps; ++k) {
             prof_begin(p, EBRL_K_OTHER);
             embed_rows(p->bf16, p->e_act, c.n_bins, c.d, out_tokens, nullptr, ntok, k - 1, nullptr, p->X, c.d, n,
-                       p->stream);
+                       p->stream, fold ? p->Xn : nullptr, c.d);
             prof_end(p, 0, 0);
             double kv_bytes = 0;
             for (int i = 0; i < n; ++i) kv_bytes += (double)(p->envs[env_ids[i]].T + k);

@@ -20,6 +20,8 @@
 // Every tile and split choice is a function of (N, K) -- plus M >= 256 for
 // the large-M kernel -- so results do not depend on timing, on the number of
 // compute units or on how many rows a decode call holds.
+#include <type_traits>
+
 #include "kernels.h"
 
 namespace ebrl {
@@ -38,13 +40,16 @@ template <typename T> struct EpiStore {
         st4<T>(C + (size_t)m * ldc + n, a, b, c, d);
     }
 };
+// Residual add; with xb set it also stores the updated rows in bf16 (the
+// operand of a following projection that folds in the RMSNorm).
 struct EpiResid {
-    float* C; int ldc;
+    float* C; int ldc; bf16_t* xb; int ldxb;
     EBRL_DEV void operator()(int m, int n, float a, float b, float c, float d) const {
         float4* p = reinterpret_cast<float4*>(C + (size_t)m * ldc + n);
         float4 r = *p;
         r.x += a; r.y += b; r.z += c; r.w += d;
         *p = r;
+        if (xb) st4<bf16_t>(xb + (size_t)m * ldxb + n, r.x, r.y, r.z, r.w);
     }
 };
 // Output row m goes to row_base[m / group] + m % group; optionally adds a
@@ -503,11 +508,11 @@ EBRL_DEV bf16x8 dec_frag(const bf16_t* lds, int row, int c) {
     return *reinterpret_cast<const bf16x8*>(lds + (row >> 3) * 512 + ((row & 7) * 8 + (c ^ (row & 7))) * 8);
 }
 
-template <int TM, int BN, bool NTW, bool PAIRED, class Epi>
+template <int TM, int BN, bool NTW, bool NORM, bool PAIRED, class Epi>
 __global__ __launch_bounds__(256) void gemm_bf16_decode_kernel(
     const bf16_t* __restrict__ A, int lda, const bf16_t* __restrict__ W, int ldw, int M, int N,
     int K, int groups_per_split, int splits, int m_tiles, float* __restrict__ ws,
-    unsigned* __restrict__ counters, Epi epi)
+    unsigned* __restrict__ counters, float norm_eps, Epi epi)
 {
     constexpr int TN = BN / 16;
     static_assert(!PAIRED || TN % 2 == 0, "paired epilogue needs fragment pairs");
@@ -522,6 +527,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_decode_kernel(
     __shared__ __attribute__((aligned(1024))) bf16_t sW1[4 * WE];
     __shared__ __attribute__((aligned(1024))) bf16_t sX1[4 * XE];
     __shared__ int s_last;
+    __shared__ float s_ssq[NORM ? 4 : 1][NORM ? TM * 16 : 1];
     static_assert(4 * FR * 64 * 16 <= (int)(sizeof(sW0) + sizeof(sX0)), "reduction buffer");
 
     const int tid = threadIdx.x, lane = tid & 63;
@@ -556,6 +562,11 @@ __global__ __launch_bounds__(256) void gemm_bf16_decode_kernel(
     for (int i = 0; i < TM; ++i)
 #pragma unroll
         for (int j = 0; j < TN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    // NORM: per-lane sum of squares of the activation elements it reads
+    // (row i * 16 + r, chunks g and 4 + g of every K group of the wave)
+    float ssq[TM];
+#pragma unroll
+    for (int i = 0; i < TM; ++i) ssq[i] = 0.f;
     // both 32-wide steps of a K group: fragment reads first, then the MFMAs
     auto compute = [&](const bf16_t* wl, const bf16_t* xl) {
         bf16x8 wa[2][TN], xb[2][TM];
@@ -565,6 +576,21 @@ __global__ __launch_bounds__(256) void gemm_bf16_decode_kernel(
             for (int j = 0; j < TN; ++j) wa[u][j] = dec_frag(wl, j * 16 + r, u * 4 + g);
 #pragma unroll
             for (int i = 0; i < TM; ++i) xb[u][i] = dec_frag(xl, i * 16 + r, u * 4 + g);
+        }
+        if constexpr (NORM) {
+            typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+#pragma unroll
+            for (int u = 0; u < 2; ++u)
+#pragma unroll
+                for (int i = 0; i < TM; ++i) {
+                    const uint4 w4 = __builtin_bit_cast(uint4, xb[u][i]);
+                    const unsigned w[4] = {w4.x, w4.y, w4.z, w4.w};
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const bf16x2_t pr = __builtin_bit_cast(bf16x2_t, w[e]);
+                        ssq[i] = __builtin_amdgcn_fdot2_f32_bf16(pr, pr, ssq[i], false);
+                    }
+                }
         }
 #pragma unroll
         for (int u = 0; u < 2; ++u)
@@ -605,6 +631,16 @@ __global__ __launch_bounds__(256) void gemm_bf16_decode_kernel(
     for (int i = 0; i < TM; ++i)
 #pragma unroll
         for (int j = 0; j < TN; ++j) red[(i * TN + j) * 64 + lane] = acc[i][j];
+    if constexpr (NORM) {
+        // lanes r, r + 16, r + 32, r + 48 hold row r's four chunk columns
+#pragma unroll
+        for (int i = 0; i < TM; ++i) {
+            float t = ssq[i];
+            t += __shfl_xor(t, 16, 64);
+            t += __shfl_xor(t, 32, 64);
+            if (g == 0) s_ssq[wave][i * 16 + r] = t;
+        }
+    }
     __syncthreads();
     auto red_at = [&](int w, int e) -> f32x4 {
         const int idx = w * FR * 64 + e;
@@ -687,6 +723,14 @@ __global__ __launch_bounds__(256) void gemm_bf16_decode_kernel(
             const int i = f0 / TN, j = f0 - i * TN;
             const int m = m0 + i * 16 + (l & 15);
             const int n = n0 + j * 16 + 4 * (l >> 4);
+            if constexpr (NORM) {
+                // RMSNorm of the row, summed over the waves' K ranges in wave order
+                const int row = i * 16 + (l & 15);
+                const float ss = ((s_ssq[0][row] + s_ssq[1][row]) + s_ssq[2][row]) + s_ssq[3][row];
+                const float rs = 1.0f / sqrtf(ss / (float)K + norm_eps);
+#pragma unroll
+                for (int h = 0; h < G; ++h) v[q][h] *= rs;
+            }
             if (m < M && n < N) {
                 if constexpr (PAIRED) {
                     float gv[4] = {v[q][0][0], v[q][0][1], v[q][0][2], v[q][0][3]};
@@ -916,24 +960,33 @@ static void launch_bf16(const GemmArgs& a, const GemmPlan& p, Epi epi, hipStream
             dim3 grid(((a.N + bn - 1) / bn) * p.splits * p.m_tiles);
             hipLaunchKernelGGL(kern, grid, dim3(256), 0, s, (const bf16_t*)a.A, a.lda, (const bf16_t*)a.B,
                                a.ldb, a.M, a.N, a.K, p.steps_per_split, p.splits, p.m_tiles, a.ws,
-                               a.counters, epi);
+                               a.counters, a.norm_eps, epi);
         };
         // Non-temporal weight loads where each weight slice is read by a
         // single workgroup (one row tile) of 64-column slices: measured 5-13 %
         // faster there, slower where row tiles or narrow slices re-read it.
-        if (p.dbn == 32) {
-            if (p.tm == 1) godec(gemm_bf16_decode_kernel<1, 32, false, PAIRED, Epi>, 32);
-            else if (p.tm == 2) godec(gemm_bf16_decode_kernel<2, 32, false, PAIRED, Epi>, 32);
-            else godec(gemm_bf16_decode_kernel<4, 32, false, PAIRED, Epi>, 32);
-        } else if (p.m_tiles == 1) {
-            if (p.tm == 1) godec(gemm_bf16_decode_kernel<1, 64, true, PAIRED, Epi>, 64);
-            else if (p.tm == 2) godec(gemm_bf16_decode_kernel<2, 64, true, PAIRED, Epi>, 64);
-            else godec(gemm_bf16_decode_kernel<4, 64, true, PAIRED, Epi>, 64);
-        } else {
-            if (p.tm == 1) godec(gemm_bf16_decode_kernel<1, 64, false, PAIRED, Epi>, 64);
-            else if (p.tm == 2) godec(gemm_bf16_decode_kernel<2, 64, false, PAIRED, Epi>, 64);
-            else godec(gemm_bf16_decode_kernel<4, 64, false, PAIRED, Epi>, 64);
+        auto pick = [&](auto NORM) {
+            constexpr bool NM = decltype(NORM)::value;
+            if (p.dbn == 32) {
+                if (p.tm == 1) godec(gemm_bf16_decode_kernel<1, 32, false, NM, PAIRED, Epi>, 32);
+                else if (p.tm == 2) godec(gemm_bf16_decode_kernel<2, 32, false, NM, PAIRED, Epi>, 32);
+                else godec(gemm_bf16_decode_kernel<4, 32, false, NM, PAIRED, Epi>, 32);
+            } else if (p.m_tiles == 1) {
+                if (p.tm == 1) godec(gemm_bf16_decode_kernel<1, 64, true, NM, PAIRED, Epi>, 64);
+                else if (p.tm == 2) godec(gemm_bf16_decode_kernel<2, 64, true, NM, PAIRED, Epi>, 64);
+                else godec(gemm_bf16_decode_kernel<4, 64, true, NM, PAIRED, Epi>, 64);
+            } else {
+                if (p.tm == 1) godec(gemm_bf16_decode_kernel<1, 64, false, NM, PAIRED, Epi>, 64);
+                else if (p.tm == 2) godec(gemm_bf16_decode_kernel<2, 64, false, NM, PAIRED, Epi>, 64);
+                else godec(gemm_bf16_decode_kernel<4, 64, false, NM, PAIRED, Epi>, 64);
+            }
+        };
+        // the folded RMSNorm exists for the projections that follow a norm
+        // (fused QKV, gate/up) and needs the whole K in one workgroup
+        if constexpr (PAIRED) {
+            if (a.row_norm && p.splits == 1) { pick(std::true_type{}); return; }
         }
+        pick(std::false_type{});
         return;
     }
     auto go = [&](auto kern, int bm, int bn) {
@@ -1005,7 +1058,7 @@ int gemm(const GemmArgs& a, hipStream_t s) {
         if (a.bf16) return dispatch<false>(a, EpiStore<bf16_t>{(bf16_t*)a.C, a.ldc}, s);
         return dispatch<false>(a, EpiStore<float>{(float*)a.C, a.ldc}, s);
     case EPI_RESID:
-        return dispatch<false>(a, EpiResid{(float*)a.C, a.ldc}, s);
+        return dispatch<false>(a, EpiResid{(float*)a.C, a.ldc, (bf16_t*)a.xb, a.ldxb}, s);
     case EPI_REMAP:
         if (a.bf16)
             return dispatch<false>(a, EpiRemap<bf16_t>{(float*)a.C, a.ldc, a.row_base, a.group,
@@ -1024,6 +1077,12 @@ int gemm(const GemmArgs& a, hipStream_t s) {
 
 int gemm_splits(bool bf16, int M, int N, int K, size_t ws_floats, bool split_ok) {
     return plan_gemm(bf16, M, N, K, ws_floats, split_ok && M <= SPLIT_MAX_M).splits;
+}
+
+bool gemm_row_norm_ok(bool bf16, int M, int N, int K, size_t ws_floats) {
+    if (!bf16 || M > SPLIT_MAX_M || K % 64) return false;
+    const GemmPlan p = plan_gemm(true, M, N, K, ws_floats, true);
+    return p.dec && p.splits == 1;
 }
 
 size_t gemm_counter_words() {

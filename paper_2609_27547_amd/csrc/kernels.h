@@ -40,10 +40,18 @@ struct GemmArgs {
     // variant sums K in the same 64-wide steps, so results do not depend on M
     // either.
     bool split_ok = false;
+    // Decode GEMMs with a paired epilogue (EPI_QKV, EPI_SWIGLU) and one K
+    // split (gemm_row_norm_ok): A holds un-normalised rows in bf16 and every
+    // output row is scaled by 1/sqrt(mean_k A[m][k]^2 + norm_eps), i.e. the
+    // unit-gain RMSNorm of the input folded into the projection.
+    bool row_norm = false; float norm_eps = 1e-6f;
+    // EPI_RESID: also store the updated rows in bf16 here (nullable).
+    void* xb = nullptr; int ldxb = 0;
 };
 // Returns the number of K splits used (1 = single pass).
 int gemm(const GemmArgs& a, hipStream_t s);
 int gemm_splits(bool bf16, int M, int N, int K, size_t ws_floats, bool split_ok);
+bool gemm_row_norm_ok(bool bf16, int M, int N, int K, size_t ws_floats);
 size_t gemm_counter_words();
 
 // ------------------------------------------------------------- attention --
@@ -125,8 +133,10 @@ void rope_kv_write(const RopeKVArgs& a, hipStream_t s);
 
 // X[dst] = E[id] as float (id = ids[src ? src[i] : i*stride + off]; dst = dst_rows ? dst_rows[i] : i);
 // ids outside [0, n_rows_e) give zero rows.
+// xb (nullable, bf16 policies): the same rows in bf16 as well.
 void embed_rows(bool bf16, const void* E, int n_rows_e, int d, const int* ids, const int* src, int stride,
-                int off, const int* dst_rows, float* X, int ldx, int n, hipStream_t s);
+                int off, const int* dst_rows, float* X, int ldx, int n, hipStream_t s, void* xb = nullptr,
+                int ldxb = 0);
 
 // images f32 [n, cams, H, W, 3] -> patches [n*cams*(H/P)*(W/P), kpad] (zero-padded columns)
 void im2col(bool bf16, const float* img, int n, int cams, int H, int W, int P, void* out,

@@ -171,29 +171,37 @@ void rope_kv_write(const RopeKVArgs& a, hipStream_t s) {
 template <typename T>
 __global__ __launch_bounds__(256) void embed_kernel(const T* E, int n_rows_e, int d, const int* ids,
                                                     const int* src, int stride, int off, const int* dst_rows,
-                                                    float* X, int ldx)
+                                                    float* X, int ldx, bf16_t* xb, int ldxb)
 {
     const int i = blockIdx.x;
     const int id = ids[src ? src[i] : i * stride + off];
     const int dst = dst_rows ? dst_rows[i] : i;
     float* x = X + (size_t)dst * ldx;
+    bf16_t* y = xb ? xb + (size_t)dst * ldxb : nullptr;
     if (id < 0 || id >= n_rows_e) {  // out-of-range ids embed as zero rows
-        for (int j = threadIdx.x; j < d; j += blockDim.x) x[j] = 0.f;
+        for (int j = threadIdx.x; j < d; j += blockDim.x) {
+            x[j] = 0.f;
+            if (y) y[j] = 0;
+        }
         return;
     }
     const T* e = E + (size_t)id * d;
-    for (int j = threadIdx.x; j < d; j += blockDim.x) x[j] = ld_elem<T>(e + j);
+    for (int j = threadIdx.x; j < d; j += blockDim.x) {
+        const float v = ld_elem<T>(e + j);
+        x[j] = v;
+        if (y) st_elem<bf16_t>(y + j, v);
+    }
 }
 
 void embed_rows(bool bf16, const void* E, int n_rows_e, int d, const int* ids, const int* src, int stride,
-                int off, const int* dst_rows, float* X, int ldx, int n, hipStream_t s) {
+                int off, const int* dst_rows, float* X, int ldx, int n, hipStream_t s, void* xb, int ldxb) {
     if (n <= 0) return;
     if (bf16)
         hipLaunchKernelGGL(embed_kernel<bf16_t>, dim3(n), dim3(256), 0, s, (const bf16_t*)E, n_rows_e, d,
-                           ids, src, stride, off, dst_rows, X, ldx);
+                           ids, src, stride, off, dst_rows, X, ldx, (bf16_t*)xb, ldxb);
     else
         hipLaunchKernelGGL(embed_kernel<float>, dim3(n), dim3(256), 0, s, (const float*)E, n_rows_e, d,
-                           ids, src, stride, off, dst_rows, X, ldx);
+                           ids, src, stride, off, dst_rows, X, ldx, (bf16_t*)nullptr, 0);
 }
 
 // ----------------------------------------------------------- patchify --

@@ -505,3 +505,36 @@ def test_bf16_emulation_rounds_only_at_storage_points():
     # equal scores: every numerator is 2^(x - ceil x) rounded alike -> mean of V
     same = M.Policy._attention_bf16(np.zeros((3, 1, 16)), k[:4], v[:4], np.arange(3) + 9, kp[:4], True)
     assert np.allclose(same, np.repeat(v[:4].mean(0, keepdims=True), 3, axis=0), atol=1e-15)
+
+
+def test_bf16_emulation_folded_prenorm():
+    # Folding the unit-gain RMSNorm into the projection is exact without
+    # rounding: x W^T / rms(x) = (x / rms(x)) W^T.  Emulating bf16, the folded
+    # operand is a bf16 value and the factor is the RMSNorm of that rounded
+    # row; the folded and unfolded emulations differ only by rounding.
+    cfg16 = tiny_cfg(bf16=True)
+    e = M.Policy(cfg16, seed=0, emulate_bf16=True)
+    rng = np.random.default_rng(3)
+    x = rng.normal(size=(3, cfg16.d)) * np.array([[0.5], [2.0], [30.0]])
+    h, f = e._prenorm(x, True)
+    assert np.array_equal(M.f64_to_bf16_value(h), h)
+    assert np.allclose(f[:, 0], 1.0 / np.sqrt(np.mean(h * h, axis=-1) + cfg16.eps), rtol=1e-15)
+    hu, fu = e._prenorm(x, False)
+    assert fu == 1.0
+    W = M.f64_to_bf16_value(rng.normal(size=(8, cfg16.d)) * 0.02)
+    y_f, y_u = M.linear(h, W) * f, M.linear(hu, W)
+    exact = M.linear(M.rmsnorm(x, cfg16.eps), W)
+    for y in (y_f, y_u):
+        rel = np.linalg.norm(y - exact, axis=-1) / np.linalg.norm(exact, axis=-1)
+        assert np.all(rel < 2.0 ** -7) and np.all(rel > 0)
+    # without emulation the fold is the identity
+    x_h, x_f = M.Policy(cfg16, seed=0)._prenorm(x, True)
+    assert x_f == 1.0 and np.array_equal(x_h, M.rmsnorm(x, cfg16.eps))
+    # a whole emulated decode stays within rounding of the exact one
+    img, lang = _obs(cfg16, [0])
+    st_e = e.prefill(img[0], lang[0])
+    a = M.Policy(cfg16, seed=0)
+    st_a = a.prefill(img[0], lang[0])
+    ra = a.decode(st_a)
+    re = e.decode(st_e, forced=ra.tokens[:-1])
+    assert np.max(np.abs(re.logits - ra.logits)) < 5e-2 * np.max(np.abs(ra.logits))
