@@ -94,6 +94,28 @@ def cpu_baseline(workload: str, n_sample: int):
             "seconds": round(dt, 3)}
 
 
+def stream_read_gbs(E, torch, stream_ptr, nbytes: int = 1 << 30) -> float:
+    """HBM read bandwidth of the library's streaming-read reference kernel on
+    the given stream (so under that stream's CU mask): the ceiling the
+    partitions' HBM-bound kernels are compared against."""
+    x = torch.empty(nbytes // 4, dtype=torch.int32, device="cuda")
+    x.fill_(1)
+    o = torch.zeros(1, dtype=torch.int32, device="cuda")
+    ext = torch.cuda.ExternalStream(stream_ptr)
+    torch.cuda.synchronize()
+    for _ in range(2):
+        E.op_stream_read(x, o, stream_ptr)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(ext)
+    for _ in range(5):
+        E.op_stream_read(x, o, stream_ptr)
+    e1.record(ext)
+    torch.cuda.synchronize()
+    gbs = 5 * nbytes / (e0.elapsed_time(e1) * 1e6)
+    del x, o
+    return round(gbs, 1)
+
+
 def balanced_mask(quarters: int, n_cu: int = 256):
     """CU mask words for quarters/4 of the CUs: runs of 8 CUs spread so every
     XCD gets the same share whether CUs are numbered XCD by XCD or round-robin
@@ -189,7 +211,7 @@ def main():
 
     torch.cuda.set_device(0)
     stream = torch.cuda.current_stream()
-    w = Workload(args.workload, E, torch, args.steps + args.warmup)
+    w = Workload(args.workload, E, torch, args.steps + args.warmup + 2)
     pol, c = w.pol, w.c
     for _ in range(args.warmup):
         w.step()
@@ -208,12 +230,16 @@ def main():
     pol.profile_read(dominant, reset=True)
     pol.profile_enable([dominant])
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    # per-step boundaries on the same stream (one event per step: the
+    # difference of consecutive ones is that step's GPU latency)
+    step_ev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     ev0.record(stream)
     actions = 0
-    for _ in range(args.steps):
+    for k in range(args.steps):
         actions += w.step()
+        step_ev[k].record(stream)
     ev1.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
@@ -222,6 +248,8 @@ def main():
     gpu_ms = ev0.elapsed_time(ev1)
     ms_per_step = 1000.0 * wall / args.steps
     actions_per_s = actions / wall
+    step_ms = np.array([ev0.elapsed_time(step_ev[0])] +
+                       [step_ev[k - 1].elapsed_time(step_ev[k]) for k in range(1, args.steps)])
 
     # ---- breakdown pass (not part of the value): every kernel class, per phase
     pol.profile_enable(classes)
@@ -252,8 +280,15 @@ def main():
 
     # ---- optional: the same steps on CU-masked partitions (the stand-in for SM quotas)
     partitions = None
+    read_bw = {}
     if args.partitions:
         partitions = {"1.00": round(actions_per_s, 2)}
+        s_all = E.create_cu_masked_stream(0, balanced_mask(4))
+        try:
+            read_bw["1.00"] = stream_read_gbs(E, torch, s_all)
+        finally:
+            torch.cuda.synchronize()
+            E.destroy_stream(s_all)
         for q in (1, 2, 3):
             s_ptr = E.create_cu_masked_stream(0, balanced_mask(q))
             try:
@@ -265,6 +300,7 @@ def main():
                 n_act = sum(w.step() for _ in range(args.steps))
                 torch.cuda.synchronize()
                 partitions[f"{q / 4:.2f}"] = round(n_act / (time.perf_counter() - t0), 2)
+                read_bw[f"{q / 4:.2f}"] = stream_read_gbs(E, torch, s_ptr)
             finally:
                 pol.bind_stream(stream.cuda_stream)
                 torch.cuda.synchronize()
@@ -335,8 +371,17 @@ def main():
         "roofline": roofline,
         "cpu_baseline": base,
     }
+    if c.exp_layers:
+        out["chunks_per_s"] = round(actions_per_s / c.chunk, 2)
+    else:
+        out["action_tokens_per_s"] = round(actions_per_s * c.n_action_tokens, 2)
+    out["step_latency_ms"] = {"p50": round(float(np.percentile(step_ms, 50)), 3),
+                              "p90": round(float(np.percentile(step_ms, 90)), 3),
+                              "p99": round(float(np.percentile(step_ms, 99)), 3),
+                              "max": round(float(step_ms.max()), 3)}
     if partitions:
         out["partitions_actions_per_s"] = partitions
+        out["partitions_stream_read_gbs"] = read_bw
     print(json.dumps(out), flush=True)
     pol.close()
 

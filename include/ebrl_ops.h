@@ -22,6 +22,17 @@ extern "C" {
 int ebrl_op_gemm(int32_t dtype, const void* A, const void* B, float* C, int32_t M, int32_t N,
                  int32_t K, void* stream);
 
+/* Reads `bytes` of device memory at `buf` once with non-temporal 16-byte
+ * loads (each workgroup a contiguous range).  Every loaded word feeds an XOR
+ * that decides whether *out (device, 4 bytes) is written, so no load can be
+ * dropped; *out is left unchanged unless that XOR equals 0x9E3779B9.  It is
+ * the streaming-read reference for HBM-bound kernels: run on a CU-masked
+ * stream it gives the bandwidth that share of the chip reaches.  Requires
+ * bytes >= 16 and bytes % 16 == 0, buf and out non-NULL and buf 16-byte
+ * aligned.  stream: hipStream_t or NULL.  Returns EBRL_E_INVALID on bad
+ * arguments. */
+int ebrl_op_stream_read(const void* buf, int64_t bytes, uint32_t* out, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

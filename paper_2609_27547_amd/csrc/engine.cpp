@@ -1321,6 +1321,12 @@ static float* g_ws = nullptr;
 static size_t g_ws_floats = 0;
 static int g_ws_dev = -1;
 
+int ebrl_op_stream_read(const void* buf, int64_t bytes, uint32_t* out, void* stream) {
+    if (!buf || !out || bytes < 16 || bytes % 16 || (uintptr_t)buf % 16) return EBRL_E_INVALID;
+    ebrl::stream_read(buf, (size_t)bytes, out, (hipStream_t)stream);
+    return hipGetLastError() == hipSuccess ? EBRL_OK : EBRL_E_HIP;
+}
+
 int ebrl_op_gemm(int32_t dtype, const void* A, const void* B, float* C, int32_t M, int32_t N, int32_t K,
                  void* stream) {
     if (!A || !B || !C || M < 1 || N < 1 || K < 8 || K % 8 || N % 4) return EBRL_E_INVALID;

@@ -159,6 +159,9 @@ struct LogitsArgs {
 };
 void action_logits(const LogitsArgs& a, hipStream_t s);
 
+// Streaming read of `bytes` (multiple of 16) with non-temporal loads (HBM read reference).
+void stream_read(const void* buf, size_t bytes, unsigned* out, hipStream_t s);
+
 // Last prefix row of each sequence: h_pre[env] = X[row]; h_norm[env] = rmsnorm(X[row]).
 void gather_last(const float* X, int ldx, const int* seq_env, const int* last_row, int n, int d,
                  float eps, float* h_pre, float* h_norm, hipStream_t s);

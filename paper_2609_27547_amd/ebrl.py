@@ -57,7 +57,7 @@ EXPORTED = [
     "ebrl_stream_create_cu_masked", "ebrl_stream_destroy", "ebrl_policy_bind_stream",
     "ebrl_prefill", "ebrl_decode_actions", "ebrl_flow_denoise", "ebrl_last_error",
     "ebrl_read_state", "ebrl_generate_weight_host", "ebrl_read_weight", "ebrl_write_weight",
-    "ebrl_profile_enable", "ebrl_profile_read", "ebrl_op_gemm",
+    "ebrl_profile_enable", "ebrl_profile_read", "ebrl_op_gemm", "ebrl_op_stream_read",
 ]
 
 
@@ -91,6 +91,7 @@ def lib():
         "ebrl_profile_read": (i32, [vp, i32, ctypes.POINTER(i64), ctypes.POINTER(ctypes.c_double),
                                     ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double), i32]),
         "ebrl_op_gemm": (i32, [i32, vp, vp, vp, i32, i32, i32, vp]),
+        "ebrl_op_stream_read": (i32, [vp, i64, vp, vp]),
     }
     for name, (res, args) in sig.items():
         f = getattr(L, name)
@@ -135,6 +136,15 @@ def op_gemm(A, B, C, stream=None) -> None:
     rc = lib().ebrl_op_gemm(dt, A.data_ptr(), B.data_ptr(), C.data_ptr(), M, N, K, s)
     if rc != EBRL_OK:
         raise EbrlError(rc, "ebrl_op_gemm")
+
+
+def op_stream_read(buf, out, stream=None) -> None:
+    """Streaming read of a device tensor's bytes (the HBM read reference)."""
+    import torch
+    s = stream if stream is not None else torch.cuda.current_stream().cuda_stream
+    rc = lib().ebrl_op_stream_read(buf.data_ptr(), buf.numel() * buf.element_size(), out.data_ptr(), s)
+    if rc != EBRL_OK:
+        raise EbrlError(rc, "ebrl_op_stream_read")
 
 
 def create_cu_masked_stream(device: int, mask_words: Sequence[int]) -> int:

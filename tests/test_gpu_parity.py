@@ -287,3 +287,18 @@ def test_tiny_vit_bf16_parity():
         assert P.row_rel_err(k.reshape(st.T, -1), st.k[0].reshape(st.T, -1)) < P.TOL_BF16
         P.check_tokens(tok[i], ref.decode(st, forced=tok[i, :-1]))
     pol.close()
+
+
+def test_stream_read_reference_kernel():
+    # the HBM read reference: argument checks, and a run that reads every
+    # byte without writing its output (the fold of 1-filled words is not the
+    # trigger constant)
+    x = torch.ones(1 << 20, dtype=torch.int32, device="cuda")
+    o = torch.full((1,), 7, dtype=torch.int32, device="cuda")
+    E.op_stream_read(x, o)
+    torch.cuda.synchronize()
+    assert int(o.item()) == 7
+    with pytest.raises(E.EbrlError) as ex:
+        E.op_stream_read(x[:3], o)                  # 12 bytes: not a multiple of 16
+    assert ex.value.code == -1
+    assert E.lib().ebrl_op_stream_read(None, 16, o.data_ptr(), None) == -1
