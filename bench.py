@@ -127,6 +127,128 @@ def balanced_mask(quarters: int, n_cu: int = 256):
     return words
 
 
+# The co-located training stand-in: one bf16 projection of a training step
+# over 8192 tokens at the 7B-class width (M x N x K), run back to back.
+LOAD_MNK = (8192, 4096, 4096)
+
+
+def _events(torch, n):
+    return [torch.cuda.Event(enable_timing=True) for _ in range(n)]
+
+
+class _GemmLoad:
+    """Keeps `depth` GEMMs queued on one stream from a host thread until
+    stopped, with a timing event after each (their completion times)."""
+
+    def __init__(self, E, torch, s_ptr, A, B, C, depth=4):
+        import threading
+        self.E, self.torch, self.s_ptr, self.A, self.B, self.C, self.depth = E, torch, s_ptr, A, B, C, depth
+        self.events = []
+        self.stop = threading.Event()
+        self.started = threading.Event()
+        self.error = None
+        self.thread = threading.Thread(target=self._run, daemon=True)
+
+    def _run(self):
+        torch = self.torch
+        try:
+            torch.cuda.set_device(0)
+            ext = torch.cuda.ExternalStream(self.s_ptr)
+            k = 0
+            while not self.stop.is_set():
+                self.E.op_gemm(self.A, self.B, self.C, self.s_ptr)
+                ev = torch.cuda.Event(enable_timing=True)
+                ev.record(ext)
+                self.events.append(ev)
+                k += 1
+                if k > self.depth:
+                    self.events[k - 1 - self.depth].synchronize()
+                    self.started.set()
+        except Exception as e:  # reported by the caller
+            self.error = e
+            self.started.set()
+
+    def __enter__(self):
+        self.thread.start()
+        self.started.wait(timeout=60)
+        return self
+
+    def __exit__(self, *exc):
+        self.stop.set()
+        self.thread.join(timeout=120)
+        if self.error:
+            raise self.error
+
+
+def colocated(E, torch, w, args):
+    """Generation on a CU-masked stream while the GEMM load runs on the
+    complementary CUs (the paper's generation and training sharing one GPU
+    under separate SM quotas), against each of the two alone on the same
+    masks.  Generation is timed by events on its stream; the load's rate is
+    taken from the completion events of its GEMMs inside the generation
+    window."""
+    Mg, Ng, Kg = LOAD_MNK
+    flop = 2.0 * Mg * Ng * Kg
+    A = torch.randn(Mg, Kg, device="cuda").to(torch.bfloat16)
+    B = torch.randn(Ng, Kg, device="cuda").to(torch.bfloat16)
+    C = torch.empty(Mg, Ng, device="cuda", dtype=torch.float32)
+    res = {"load": f"bf16 GEMM {Mg} x {Ng} x {Kg} through ebrl_op_gemm, kept queued on the complementary CUs"}
+
+    def gen_run(s_ptr):
+        ext_g = torch.cuda.ExternalStream(s_ptr)
+        if args.workload == "ragged-7b":
+            w.call_i = args.warmup
+        g0, g1 = _events(torch, 2)
+        g0.record(ext_g)
+        n_act = 0
+        for _ in range(args.steps):
+            n_act += w.step()
+        g1.record(ext_g)
+        g1.synchronize()
+        ms = g0.elapsed_time(g1)
+        return n_act / (ms / 1000.0), ms, g0
+
+    for q in (1, 2, 3):
+        gmask = balanced_mask(q)
+        lmask = [(~x) & 0xFFFFFFFF for x in gmask]
+        s_gen = E.create_cu_masked_stream(0, gmask)
+        s_load = E.create_cu_masked_stream(0, lmask)
+        try:
+            w.pol.bind_stream(s_gen)
+            torch.cuda.synchronize()
+            gen_iso, _, _ = gen_run(s_gen)
+            torch.cuda.synchronize()
+            with _GemmLoad(E, torch, s_load, A, B, C) as ld:
+                t_ld = time.perf_counter()
+                time.sleep(0.05)
+                n0 = len(ld.events)
+                gen_co, gen_ms, g0 = gen_run(s_gen)
+            torch.cuda.synchronize()
+            iso_ev = ld.events[max(1, n0 // 2):n0]          # the load alone, before generation started
+            t_ev = [g0.elapsed_time(e) for e in ld.events[n0:]]
+            inside = [t for t in t_ev if 0.0 <= t <= gen_ms]
+            load_co = (len(inside) - 1) * flop / ((inside[-1] - inside[0]) * 1e9) if len(inside) >= 2 else None
+            load_iso = ((len(iso_ev) - 1) * flop / (iso_ev[0].elapsed_time(iso_ev[-1]) * 1e9)
+                        if len(iso_ev) >= 2 else None)
+            res[f"{q / 4:.2f}"] = {
+                "gen_isolated_actions_per_s": round(gen_iso, 2),
+                "gen_colocated_actions_per_s": round(gen_co, 2),
+                "gen_colocated_over_isolated": round(gen_co / gen_iso, 3),
+                "load_isolated_tflops": round(load_iso, 1) if load_iso else None,
+                "load_colocated_tflops": round(load_co, 1) if load_co else None,
+                "load_gemms_during_gen": len(inside),
+                "load_covered_gen": bool(t_ev) and t_ev[-1] > gen_ms,
+            }
+            log(f"colocated {q / 4:.2f}: {res[f'{q / 4:.2f}']} (load thread up {time.perf_counter() - t_ld:.2f} s)")
+        finally:
+            w.pol.bind_stream(torch.cuda.current_stream().cuda_stream)
+            torch.cuda.synchronize()
+            E.destroy_stream(s_gen)
+            E.destroy_stream(s_load)
+    del A, B, C
+    return res
+
+
 class Workload:
     """Sets up one workload's policy and resident inputs; step() enqueues
     one pass of the hot path and returns the actions it produces."""
@@ -199,6 +321,8 @@ def main():
                     help="envs in the oracle sample (0 = skip; default: about 10-40 s of oracle work)")
     ap.add_argument("--partitions", action="store_true",
                     help="also time the steps on CU-masked streams of 25/50/75%% of the CUs")
+    ap.add_argument("--colocate", action="store_true",
+                    help="also time generation on 25/50/75%% of the CUs beside a GEMM load on the rest")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: measures one GPU only (asked for --gpus {args.gpus}); environments are "
@@ -306,6 +430,8 @@ def main():
                 torch.cuda.synchronize()
                 E.destroy_stream(s_ptr)
 
+    coloc = colocated(E, torch, w, args) if args.colocate else None
+
     bf16 = pol.bf16
     if dominant in (E.K_GEMM, E.K_ATTN_PREFILL):
         peak = PEAK_BF16_TFLOPS if bf16 else PEAK_FP32_TFLOPS
@@ -382,6 +508,8 @@ def main():
     if partitions:
         out["partitions_actions_per_s"] = partitions
         out["partitions_stream_read_gbs"] = read_bw
+    if coloc:
+        out["colocated"] = coloc
     print(json.dumps(out), flush=True)
     pol.close()
 

@@ -231,6 +231,51 @@ def test_small_bf16_sampled_envs(small, env):
     P.check_tokens(tok[env], ref.decode(st, forced=tok[env, :-1]))
 
 
+def _half_masks():
+    """Two complementary CU masks of 128 CUs each, 8-CU runs alternating so
+    both halves hold the same share of every XCD."""
+    a = [0] * 8
+    for i in range(256):
+        if (i // 8) % 2 == 0:
+            a[i // 32] |= 1 << (i % 32)
+    return a, [(~x) & 0xFFFFFFFF for x in a]
+
+
+def test_small_bf16_decode_bitwise_beside_gemm_load(small):
+    # generation on half the CUs while GEMMs (the co-located trainer's
+    # stand-in) keep the other half busy: outputs bitwise equal to the run on
+    # the whole GPU -- no tile, split or reduction choice depends on the CUs
+    # available or on timing
+    cfg, ids, img, lang, pol, tok, ref = small
+    tok_f, act_f, mar_f = pol.decode_actions(ids)
+    torch.cuda.synchronize()
+    gmask, lmask = _half_masks()
+    s_gen = E.create_cu_masked_stream(0, gmask)
+    s_load = E.create_cu_masked_stream(0, lmask)
+    A = torch.randn(2048, 4096, device="cuda").to(torch.bfloat16)
+    B = torch.randn(4096, 4096, device="cuda").to(torch.bfloat16)
+    C = torch.empty(2048, 4096, device="cuda", dtype=torch.float32)
+    try:
+        pol.bind_stream(s_gen)
+        for rep in range(3):
+            for _ in range(96):                     # about 8 ms on half the chip
+                E.op_gemm(A, B, C, s_load)
+            done = torch.cuda.Event()
+            done.record(torch.cuda.ExternalStream(s_load))
+            tok2, act2, mar2 = pol.decode_actions(ids)
+            torch.cuda.ExternalStream(s_gen).synchronize()
+            overlapped = not done.query()
+            torch.cuda.synchronize()
+            print(f"rep {rep}: load still running when decode finished: {overlapped}", flush=True)
+            assert torch.equal(tok2, tok_f) and torch.equal(act2, act_f) and torch.equal(mar2, mar_f)
+        assert np.array_equal(tok_f.cpu().numpy(), tok)
+    finally:
+        pol.bind_stream(torch.cuda.current_stream().cuda_stream)
+        torch.cuda.synchronize()
+        E.destroy_stream(s_gen)
+        E.destroy_stream(s_load)
+
+
 # ------------------------------------------------------------ tiny flow --
 
 TINY_FLOW = M.Config("tinyflow", bf16=True, n_cams=1, img=32, patch=16, layers=2, d=128, q_heads=4,
