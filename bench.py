@@ -249,6 +249,91 @@ def colocated(E, torch, w, args):
     return res
 
 
+def gen_profile(E, torch, w, args, batches=(16, 32, 64, 128), quarters=(1, 2, 3, 4), calls=8):
+    """P_gen(s, B) of Section 4.3.2 measured on this GPU: actions/s of decode
+    calls of exactly B envs on a stream masked to s of the CUs (one action,
+    i.e. one rollout chunk-step, per env per call)."""
+    table = np.zeros((len(quarters), len(batches)))
+    for i, q in enumerate(quarters):
+        s_ptr = E.create_cu_masked_stream(0, balanced_mask(q))
+        try:
+            w.pol.bind_stream(s_ptr)
+            ext = torch.cuda.ExternalStream(s_ptr)
+            for j, b in enumerate(batches):
+                ids = list(range(b))
+                tok, act = w.tok[:b], w.act[:b]
+                for _ in range(2):
+                    w.pol.decode_actions(ids, tokens=tok, actions=act, margins=None, with_margin=False)
+                e0, e1 = _events(torch, 2)
+                e0.record(ext)
+                for _ in range(calls):
+                    w.pol.decode_actions(ids, tokens=tok, actions=act, margins=None, with_margin=False)
+                e1.record(ext)
+                e1.synchronize()
+                table[i, j] = calls * b / (e0.elapsed_time(e1) / 1000.0)
+        finally:
+            w.pol.bind_stream(torch.cuda.current_stream().cuda_stream)
+            torch.cuda.synchronize()
+            E.destroy_stream(s_ptr)
+    return [25 * q for q in quarters], list(batches), table
+
+
+def load_profile(E, torch, quarters=(1, 2, 3, 4), reps=6):
+    """TFLOP/s of the training stand-in GEMM alone on each CU share."""
+    Mg, Ng, Kg = LOAD_MNK
+    A = torch.randn(Mg, Kg, device="cuda").to(torch.bfloat16)
+    B = torch.randn(Ng, Kg, device="cuda").to(torch.bfloat16)
+    C = torch.empty(Mg, Ng, device="cuda", dtype=torch.float32)
+    out = []
+    for q in quarters:
+        s_ptr = E.create_cu_masked_stream(0, balanced_mask(q))
+        try:
+            ext = torch.cuda.ExternalStream(s_ptr)
+            for _ in range(2):
+                E.op_gemm(A, B, C, s_ptr)
+            e0, e1 = _events(torch, 2)
+            e0.record(ext)
+            for _ in range(reps):
+                E.op_gemm(A, B, C, s_ptr)
+            e1.record(ext)
+            e1.synchronize()
+            out.append(reps * 2.0 * Mg * Ng * Kg / (e0.elapsed_time(e1) * 1e9))
+        finally:
+            torch.cuda.synchronize()
+            E.destroy_stream(s_ptr)
+    del A, B, C
+    return out
+
+
+def allocation(E, torch, w, args):
+    """Algorithm 1 of Section 4.3.2 on tables measured here (generation, and
+    the GEMM stand-in for training) plus a modelled CPU simulator.  Model
+    numbers, stated so the result can be read: a training chunk-step costs
+    6 x 6.5e9 x 295 FLOP (forward and backward of the 7B-class decoder over
+    one 288-token prefix plus its 7 action tokens) at the stand-in GEMM's
+    measured rate; the simulator steps an environment in 40 ms on one core
+    (the paper's average step time, Section 3.2) or 28 ms on two, with 64 host
+    cores, and needs no GPU; device memory is 288 GB, of which generation
+    holds its 14 GB of weights plus 168 MB of KV per env and training 120 GB
+    (weights, gradients, Adam state) plus 2 GB per sample of its batch."""
+    quotas, batches, gen = gen_profile(E, torch, w, args)
+    tflops = load_profile(E, torch)
+    flop_per_sample = 6 * 6.5e9 * 295
+    train = np.array([[t * 1e12 / flop_per_sample] for t in tflops])
+    P = dict(cenv=np.array([1, 2]), ssim=np.array([0]), sim=np.array([[64 / 0.040], [32 / 0.028]]),
+             sgen=np.array(quotas), bgen=np.array(batches), gen=gen,
+             gen_mem=np.array([14e9 + 168e6 * b for b in batches]),
+             strain=np.array(quotas), btrain=np.array([32]), train=train,
+             train_mem=np.array([120e9 + 2e9 * 32]))
+    res = E.alloc_solve(P, cores=64, mem_bytes=288e9, sgen_min=10, strain_min=10)
+    return {"gen_quota_pct": quotas, "gen_batch": batches,
+            "P_gen_actions_per_s": [[round(x, 1) for x in row] for row in gen],
+            "train_standin_tflops": [round(t, 1) for t in tflops],
+            "P_train_chunk_steps_per_s": [round(x, 2) for x in train[:, 0]],
+            "P_sim_chunk_steps_per_s": {"1 core/env": 1600.0, "2 cores/env": round(32 / 0.028, 1)},
+            "result": {k: (round(v, 2) if isinstance(v, float) else v) for k, v in res.items()}}
+
+
 class Workload:
     """Sets up one workload's policy and resident inputs; step() enqueues
     one pass of the hot path and returns the actions it produces."""
@@ -321,6 +406,8 @@ def main():
                     help="envs in the oracle sample (0 = skip; default: about 10-40 s of oracle work)")
     ap.add_argument("--partitions", action="store_true",
                     help="also time the steps on CU-masked streams of 25/50/75%% of the CUs")
+    ap.add_argument("--allocate", action="store_true",
+                    help="ragged-7b only: measure P_gen on CU shares and run the elastic allocator on it")
     ap.add_argument("--colocate", action="store_true",
                     help="also time generation on 25/50/75%% of the CUs beside a GEMM load on the rest")
     args = ap.parse_args()
@@ -431,6 +518,7 @@ def main():
                 E.destroy_stream(s_ptr)
 
     coloc = colocated(E, torch, w, args) if args.colocate else None
+    alloc = allocation(E, torch, w, args) if args.allocate and args.workload == "ragged-7b" else None
 
     bf16 = pol.bf16
     if dominant in (E.K_GEMM, E.K_ATTN_PREFILL):
@@ -510,6 +598,8 @@ def main():
         out["partitions_stream_read_gbs"] = read_bw
     if coloc:
         out["colocated"] = coloc
+    if alloc:
+        out["allocation"] = alloc
     print(json.dumps(out), flush=True)
     pol.close()
 

@@ -1,7 +1,7 @@
 """Build the GPU library libebrl.so for gfx950 (in-tree).
 
 Every HIP source is compiled with hipcc for gfx950; the host-side weight
-generator with g++.  Objects go to _build/ (not committed).
+generator and resource allocator with g++.  Objects go to _build/ (not committed).
 """
 from __future__ import annotations
 
@@ -22,7 +22,7 @@ HIP_FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
              "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
              "-Wno-unused-result", "-I", os.path.join(ROOT, "include")]
 HIP_SOURCES = ["gemm.hip", "attention.hip", "misc.hip", "engine.cpp"]
-CXX_SOURCES = ["weights.cpp"]
+CXX_SOURCES = ["weights.cpp", "alloc.cpp"]
 
 
 def _run(cmd, verbose):
@@ -45,7 +45,7 @@ def build(verbose: bool = False) -> str:
         objs.append(obj)
     for src in CXX_SOURCES:
         obj = os.path.join(BUILD, src.replace(".", "_") + ".o")
-        cmd = ["g++", "-O2", "-std=c++17", "-fPIC", "-ffp-contract=off", "-c",
+        cmd = ["g++", "-O2", "-std=c++17", "-fPIC", "-ffp-contract=off", "-I", os.path.join(ROOT, "include"), "-c",
                os.path.join(CSRC, src), "-o", obj]
         jobs.append(cmd)
         objs.append(obj)

@@ -1,4 +1,4 @@
-"""Thin Python binding of the C ABI in include/ebrl.h (argument marshalling only).
+"""Thin Python binding of the C ABI in include/*.h (argument marshalling only).
 
 Every step of the policy forward runs in libebrl.so's HIP kernels; this
 module only passes device pointers (from torch tensors), host id arrays and
@@ -44,6 +44,30 @@ class ObsBatch(ctypes.Structure):
                 ("lang_len", ctypes.c_void_p), ("lang_stride", _I32)]
 
 
+_PI32, _PF64 = ctypes.POINTER(_I32), ctypes.POINTER(ctypes.c_double)
+
+
+class AllocProfiles(ctypes.Structure):
+    _fields_ = [("n_cenv", _I32), ("cenv", _PI32), ("n_ssim", _I32), ("ssim", _PI32), ("sim_rate", _PF64),
+                ("n_sgen", _I32), ("sgen", _PI32), ("n_bgen", _I32), ("bgen", _PI32), ("gen_rate", _PF64),
+                ("gen_mem", _PF64),
+                ("n_strain", _I32), ("strain", _PI32), ("n_btrain", _I32), ("btrain", _PI32),
+                ("train_rate", _PF64), ("train_mem", _PF64)]
+
+
+class AllocLimits(ctypes.Structure):
+    _fields_ = [("cores", _I32), ("mem_bytes", ctypes.c_double), ("sgen_min", _I32), ("strain_min", _I32),
+                ("knee_tol", ctypes.c_double)]
+
+
+class AllocResult(ctypes.Structure):
+    _fields_ = [(n, _I32) for n in ("cenv", "envs", "ssim", "sgen", "strain", "bgen", "btrain", "iterations")] + \
+               [(n, ctypes.c_double) for n in ("t_sim", "t_gen", "t_train", "t_rollout", "theta")]
+
+    def as_dict(self):
+        return {n: getattr(self, n) for n, _ in self._fields_}
+
+
 class EbrlError(RuntimeError):
     def __init__(self, code, msg):
         super().__init__(f"{ERRORS.get(code, code)}: {msg}")
@@ -58,6 +82,8 @@ EXPORTED = [
     "ebrl_prefill", "ebrl_decode_actions", "ebrl_flow_denoise", "ebrl_last_error",
     "ebrl_read_state", "ebrl_generate_weight_host", "ebrl_read_weight", "ebrl_write_weight",
     "ebrl_profile_enable", "ebrl_profile_read", "ebrl_op_gemm", "ebrl_op_stream_read",
+    "ebrl_alloc_solve", "ebrl_alloc_objective", "ebrl_alloc_monitor_create", "ebrl_alloc_monitor_observe",
+    "ebrl_alloc_monitor_destroy", "ebrl_alloc_refine",
 ]
 
 
@@ -92,6 +118,14 @@ def lib():
                                     ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double), i32]),
         "ebrl_op_gemm": (i32, [i32, vp, vp, vp, i32, i32, i32, vp]),
         "ebrl_op_stream_read": (i32, [vp, i64, vp, vp]),
+        "ebrl_alloc_solve": (i32, [ctypes.POINTER(AllocProfiles), ctypes.POINTER(AllocLimits),
+                                   ctypes.POINTER(AllocResult)]),
+        "ebrl_alloc_objective": (i32, [ctypes.POINTER(AllocProfiles), ctypes.POINTER(AllocResult)]),
+        "ebrl_alloc_monitor_create": (i32, [i32, ctypes.c_double, i32, ctypes.POINTER(vp)]),
+        "ebrl_alloc_monitor_observe": (i32, [vp, ctypes.c_double, ctypes.c_double, pI32]),
+        "ebrl_alloc_monitor_destroy": (None, [vp]),
+        "ebrl_alloc_refine": (i32, [ctypes.POINTER(AllocProfiles), ctypes.POINTER(AllocResult), ctypes.c_double,
+                                    ctypes.c_double, _PF64, _PF64]),
     }
     for name, (res, args) in sig.items():
         f = getattr(L, name)
@@ -116,6 +150,105 @@ def _ids(env_ids) -> ctypes.Array:
 
 def _ptr(t) -> Optional[int]:
     return None if t is None else int(t.data_ptr())
+
+
+# ---------------------------------------------------- resource allocator --
+
+def _alloc_profiles(P: dict):
+    """Marshals a profile dict (cenv, ssim, sim[C, S], sgen, bgen, gen[G, Bg],
+    gen_mem, strain, btrain, train[H, Bt], train_mem) into the C struct;
+    returns the struct and the arrays it points into (kept alive by the
+    caller)."""
+    keep = {}
+
+    def i32(k):
+        keep[k] = np.ascontiguousarray(np.asarray(P[k], dtype=np.int32))
+        return len(keep[k]), keep[k].ctypes.data_as(_PI32)
+
+    def f64(k):
+        keep[k] = np.ascontiguousarray(np.asarray(P[k], dtype=np.float64))
+        return keep[k].ctypes.data_as(_PF64)
+
+    pr = AllocProfiles()
+    pr.n_cenv, pr.cenv = i32("cenv")
+    pr.n_ssim, pr.ssim = i32("ssim")
+    pr.sim_rate = f64("sim")
+    pr.n_sgen, pr.sgen = i32("sgen")
+    pr.n_bgen, pr.bgen = i32("bgen")
+    pr.gen_rate, pr.gen_mem = f64("gen"), f64("gen_mem")
+    pr.n_strain, pr.strain = i32("strain")
+    pr.n_btrain, pr.btrain = i32("btrain")
+    pr.train_rate, pr.train_mem = f64("train"), f64("train_mem")
+    for k, shape in (("sim", (pr.n_cenv, pr.n_ssim)), ("gen", (pr.n_sgen, pr.n_bgen)),
+                     ("train", (pr.n_strain, pr.n_btrain))):
+        if keep[k].shape != shape:
+            raise EbrlError(-1, f"profile table {k} has shape {keep[k].shape}, expected {shape}")
+    for k, n in (("gen_mem", pr.n_bgen), ("train_mem", pr.n_btrain)):
+        if keep[k].shape != (n,):
+            raise EbrlError(-1, f"{k} has shape {keep[k].shape}, expected ({n},)")
+    return pr, keep
+
+
+def alloc_solve(P: dict, cores: int, mem_bytes: float, sgen_min: int, strain_min: int,
+                knee_tol: float = 0.05) -> dict:
+    """Algorithm 1 through the library (include/ebrl_alloc.h)."""
+    pr, keep = _alloc_profiles(P)
+    lim = AllocLimits(cores, mem_bytes, sgen_min, strain_min, knee_tol)
+    out = AllocResult()
+    rc = lib().ebrl_alloc_solve(ctypes.byref(pr), ctypes.byref(lim), ctypes.byref(out))
+    if rc != EBRL_OK:
+        raise EbrlError(rc, "ebrl_alloc_solve")
+    return out.as_dict()
+
+
+def alloc_objective(P: dict, cfg: dict) -> dict:
+    pr, keep = _alloc_profiles(P)
+    out = AllocResult(**{k: cfg[k] for k in ("sgen", "strain", "bgen", "btrain", "t_sim")})
+    rc = lib().ebrl_alloc_objective(ctypes.byref(pr), ctypes.byref(out))
+    if rc != EBRL_OK:
+        raise EbrlError(rc, "ebrl_alloc_objective")
+    return out.as_dict()
+
+
+def alloc_refine(P: dict, cur: dict, observed_gen: float, observed_train: float):
+    pr, keep = _alloc_profiles(P)
+    res = AllocResult(**{k: cur[k] for k in ("bgen", "btrain", "t_gen", "t_train")})
+    gen = np.empty_like(keep["gen"])
+    train = np.empty_like(keep["train"])
+    rc = lib().ebrl_alloc_refine(ctypes.byref(pr), ctypes.byref(res), observed_gen, observed_train,
+                                 gen.ctypes.data_as(_PF64), train.ctypes.data_as(_PF64))
+    if rc != EBRL_OK:
+        raise EbrlError(rc, "ebrl_alloc_refine")
+    return gen, train
+
+
+class AllocMonitor:
+    """The runtime adaptation trigger (ebrl_alloc_monitor_*)."""
+
+    def __init__(self, window: int = 20, gap: float = 0.15, patience: int = 20):
+        h = ctypes.c_void_p()
+        rc = lib().ebrl_alloc_monitor_create(window, gap, patience, ctypes.byref(h))
+        if rc != EBRL_OK:
+            raise EbrlError(rc, "ebrl_alloc_monitor_create")
+        self.h = h.value
+
+    def observe(self, rollout_rate: float, train_rate: float) -> bool:
+        t = _I32()
+        rc = lib().ebrl_alloc_monitor_observe(self.h, rollout_rate, train_rate, ctypes.byref(t))
+        if rc != EBRL_OK:
+            raise EbrlError(rc, "ebrl_alloc_monitor_observe")
+        return bool(t.value)
+
+    def close(self):
+        if self.h:
+            lib().ebrl_alloc_monitor_destroy(self.h)
+            self.h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
 
 
 def generate_weight_host(seed: int, tensor_id: int, count: int, std: float, bf16: bool) -> np.ndarray:
