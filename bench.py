@@ -334,6 +334,44 @@ def allocation(E, torch, w, args):
             "result": {k: (round(v, 2) if isinstance(v, float) else v) for k, v in res.items()}}
 
 
+def rollout(E, torch, w, args, groups=4, chunk=8, cores=16, horizon=20.0):
+    """Section 4.2's rollout pipeline around the generation calls: the
+    library's scheduler (group pipeline + Algorithm 2 core rebinding) over a
+    discrete-event stand-in for the simulators (per-env step times with mean
+    40 ms and P99 60 ms, Section 3.2), where each group's generation is the
+    real call on this GPU -- prefill of the group's observations and flow
+    denoising of its action chunk -- timed with HIP events.  chunk actions of
+    each generated chunk are executed; time is simulated, generation time
+    measured.  The same run with envs bound to fixed cores is reported next
+    to it."""
+    import synth_inputs
+    from paper_2609_27547_amd import rollout as R
+    n = w.n
+    lat = synth_inputs.sim_step_latency(6, n, 40000)
+    ext = torch.cuda.current_stream()
+
+    def generate(ids):
+        idx = torch.as_tensor(np.asarray(ids, dtype=np.int64), device="cuda")
+        img, lang, noise = w.img.index_select(0, idx), w.lang.index_select(0, idx), w.noise.index_select(0, idx)
+        e0, e1 = _events(torch, 2)
+        e0.record(ext)
+        w.pol.prefill(list(ids), images=img, lang_ids=lang)
+        w.pol.flow_denoise(list(ids), noise)
+        e1.record(ext)
+        e1.synchronize()
+        return e0.elapsed_time(e1) / 1000.0
+
+    for g in range(groups):                     # capture the group-size graphs before timing
+        generate(list(range(g * n // groups, (g + 1) * n // groups)))
+    res = {"envs": n, "groups": groups, "chunk_actions_executed": chunk, "cores": cores,
+           "simulated_horizon_s": horizon}
+    for name, fixed in (("rebinding", False), ("fixed_binding", True)):
+        out = R.run(n, groups, chunk, cores, lat, generate, horizon, fixed_binding=fixed)
+        res[name] = {k: round(v, 4) if isinstance(v, float) else v for k, v in out.items()}
+        log(f"rollout {name}: {res[name]}")
+    return res
+
+
 class Workload:
     """Sets up one workload's policy and resident inputs; step() enqueues
     one pass of the hot path and returns the actions it produces."""
@@ -408,6 +446,8 @@ def main():
                     help="also time the steps on CU-masked streams of 25/50/75%% of the CUs")
     ap.add_argument("--allocate", action="store_true",
                     help="ragged-7b only: measure P_gen on CU shares and run the elastic allocator on it")
+    ap.add_argument("--rollout", action="store_true",
+                    help="flow-bf16 only: run the rollout scheduler with this GPU's generation calls")
     ap.add_argument("--colocate", action="store_true",
                     help="also time generation on 25/50/75%% of the CUs beside a GEMM load on the rest")
     args = ap.parse_args()
@@ -519,6 +559,7 @@ def main():
 
     coloc = colocated(E, torch, w, args) if args.colocate else None
     alloc = allocation(E, torch, w, args) if args.allocate and args.workload == "ragged-7b" else None
+    roll = rollout(E, torch, w, args) if args.rollout and args.workload == "flow-bf16" else None
 
     bf16 = pol.bf16
     if dominant in (E.K_GEMM, E.K_ATTN_PREFILL):
@@ -600,6 +641,8 @@ def main():
         out["colocated"] = coloc
     if alloc:
         out["allocation"] = alloc
+    if roll:
+        out["rollout"] = roll
     print(json.dumps(out), flush=True)
     pol.close()
 

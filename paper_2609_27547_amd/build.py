@@ -1,7 +1,7 @@
 """Build the GPU library libebrl.so for gfx950 (in-tree).
 
 Every HIP source is compiled with hipcc for gfx950; the host-side weight
-generator and resource allocator with g++.  Objects go to _build/ (not committed).
+generator, resource allocator and rollout scheduler with g++.  Objects go to _build/ (not committed).
 """
 from __future__ import annotations
 
@@ -22,7 +22,7 @@ HIP_FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
              "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
              "-Wno-unused-result", "-I", os.path.join(ROOT, "include")]
 HIP_SOURCES = ["gemm.hip", "attention.hip", "misc.hip", "engine.cpp"]
-CXX_SOURCES = ["weights.cpp", "alloc.cpp"]
+CXX_SOURCES = ["weights.cpp", "alloc.cpp", "sched.cpp"]
 
 
 def _run(cmd, verbose):

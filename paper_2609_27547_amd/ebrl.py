@@ -84,6 +84,8 @@ EXPORTED = [
     "ebrl_profile_enable", "ebrl_profile_read", "ebrl_op_gemm", "ebrl_op_stream_read",
     "ebrl_alloc_solve", "ebrl_alloc_objective", "ebrl_alloc_monitor_create", "ebrl_alloc_monitor_observe",
     "ebrl_alloc_monitor_destroy", "ebrl_alloc_refine",
+    "ebrl_sched_create", "ebrl_sched_destroy", "ebrl_sched_dispatch", "ebrl_sched_complete",
+    "ebrl_sched_next_group", "ebrl_sched_deliver", "ebrl_sched_env_state",
 ]
 
 
@@ -126,6 +128,13 @@ def lib():
         "ebrl_alloc_monitor_destroy": (None, [vp]),
         "ebrl_alloc_refine": (i32, [ctypes.POINTER(AllocProfiles), ctypes.POINTER(AllocResult), ctypes.c_double,
                                     ctypes.c_double, _PF64, _PF64]),
+        "ebrl_sched_create": (i32, [i32, i32, i32, ctypes.POINTER(vp)]),
+        "ebrl_sched_destroy": (None, [vp]),
+        "ebrl_sched_dispatch": (i32, [vp, i32, i32, pI32]),
+        "ebrl_sched_complete": (i32, [vp, i32, ctypes.c_double, pI32]),
+        "ebrl_sched_next_group": (i32, [vp, pI32, pI32, i32, pI32]),
+        "ebrl_sched_deliver": (i32, [vp, i32]),
+        "ebrl_sched_env_state": (i32, [vp, i32, pI32, pI32, pI32, _PF64]),
     }
     for name, (res, args) in sig.items():
         f = getattr(L, name)
@@ -242,6 +251,61 @@ class AllocMonitor:
     def close(self):
         if self.h:
             lib().ebrl_alloc_monitor_destroy(self.h)
+            self.h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+# ------------------------------------------------------ rollout scheduler --
+
+class Sched:
+    """The group pipeline and Algorithm 2 dispatcher (include/ebrl_sched.h)."""
+
+    def __init__(self, n_envs: int, n_groups: int, chunk_len: int):
+        h = ctypes.c_void_p()
+        rc = lib().ebrl_sched_create(n_envs, n_groups, chunk_len, ctypes.byref(h))
+        if rc != EBRL_OK:
+            raise EbrlError(rc, "ebrl_sched_create")
+        self.h = h.value
+        self.n_envs = n_envs
+        self._ids = np.empty(n_envs, dtype=np.int32)
+
+    def _check(self, rc, what):
+        if rc != EBRL_OK:
+            raise EbrlError(rc, what)
+
+    def dispatch(self, core: int = 0, bind_stride: int = 0) -> int:
+        e = _I32()
+        self._check(lib().ebrl_sched_dispatch(self.h, core, bind_stride, ctypes.byref(e)), "ebrl_sched_dispatch")
+        return e.value
+
+    def complete(self, env: int, duration: float) -> bool:
+        d = _I32()
+        self._check(lib().ebrl_sched_complete(self.h, env, duration, ctypes.byref(d)), "ebrl_sched_complete")
+        return bool(d.value)
+
+    def next_group(self):
+        g, n = _I32(), _I32()
+        self._check(lib().ebrl_sched_next_group(self.h, ctypes.byref(g), self._ids.ctypes.data_as(_PI32),
+                                                self.n_envs, ctypes.byref(n)), "ebrl_sched_next_group")
+        return g.value, self._ids[:n.value].copy()
+
+    def deliver(self, group: int) -> None:
+        self._check(lib().ebrl_sched_deliver(self.h, group), "ebrl_sched_deliver")
+
+    def env_state(self, env: int):
+        a, b, c, d = _I32(), _I32(), _I32(), ctypes.c_double()
+        self._check(lib().ebrl_sched_env_state(self.h, env, ctypes.byref(a), ctypes.byref(b), ctypes.byref(c),
+                                               ctypes.byref(d)), "ebrl_sched_env_state")
+        return a.value, bool(b.value), bool(c.value), d.value
+
+    def close(self):
+        if self.h:
+            lib().ebrl_sched_destroy(self.h)
             self.h = None
 
     def __del__(self):

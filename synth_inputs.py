@@ -122,3 +122,21 @@ def ragged_prefix_lengths(seed: int, pool: int, lo: int, hi: int) -> np.ndarray:
     """Per-slot prefix lengths uniform in [lo, hi] for the env pool."""
     rng = np.random.Generator(np.random.Philox(seed + 1))
     return rng.integers(lo, hi + 1, size=pool).astype(np.int32)
+
+
+def sim_step_latency(seed: int, n_envs: int, n_steps: int, mean: float = 0.040, p99: float = 0.060):
+    """Simulator step durations (seconds) ``[n_envs, n_steps]``: entry
+    [e, k] is env e's k-th step.  Log-normal with the given overall mean and
+    99th percentile (the paper reports 40 ms and 60 ms for its simulators'
+    step time, Section 3.2), the log-variance split evenly between a
+    persistent per-env factor (some envs are slower) and per-step noise."""
+    # log-normal: mean = exp(mu + s^2 / 2), p99 = exp(mu + 2.3263 s)
+    z99 = 2.3263478740408408
+    # solve z99 s - s^2 / 2 = ln(p99 / mean) for the smaller root
+    c = np.log(p99 / mean)
+    s = z99 - np.sqrt(z99 * z99 - 2.0 * c)
+    mu = np.log(mean) - 0.5 * s * s
+    rng = np.random.Generator(np.random.Philox(seed))
+    env = rng.normal(0.0, s / np.sqrt(2.0), size=(n_envs, 1))
+    step = rng.normal(0.0, s / np.sqrt(2.0), size=(n_envs, n_steps))
+    return np.exp(mu + env + step)
