@@ -33,10 +33,11 @@ WORKLOADS = {
     "small-bf16": (2, 64, 1002),
     "7b-bf16": (3, 32, 1003),
     "flow-bf16": (4, 64, 1004),
+    "wam-bf16": (5, 64, 1005),
     "ragged-7b": (3, 128, 1005),
 }
 # default oracle sample per workload: envs that take roughly 10-40 s on the host
-CPU_SAMPLE = {"tiny-fp32": 8, "small-bf16": 32, "7b-bf16": 1, "flow-bf16": 3, "ragged-7b": 0}
+CPU_SAMPLE = {"tiny-fp32": 8, "small-bf16": 32, "7b-bf16": 1, "flow-bf16": 3, "wam-bf16": 2, "ragged-7b": 0}
 PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA
 PEAK_FP32_TFLOPS = 157.3      # MI355X fp32 vector
 PEAK_HBM_GBS = 8000.0
@@ -82,7 +83,10 @@ def cpu_baseline(workload: str, n_sample: int):
     per_env = cfg.chunk if cfg.exp_layers else 1
     for i in ids:
         st = pol.prefill(img[i], lang[i])
-        if cfg.exp_layers:
+        if cfg.frame_tokens:
+            pol.wam_denoise(st, synth_inputs.flow_noise(5, [i], cfg.frame_tokens, cfg.frame_dim)[0],
+                            synth_inputs.flow_noise(4, [i], cfg.chunk, cfg.adim)[0])
+        elif cfg.exp_layers:
             pol.flow_denoise(st, synth_inputs.flow_noise(4, [i], cfg.chunk, cfg.adim)[0])
         else:
             pol.decode(st)
@@ -408,6 +412,9 @@ class Workload:
         if c.exp_layers:
             self.noise = dev(synth_inputs.flow_noise(4, ids, c.chunk, c.adim))
             self.out = torch.empty_like(self.noise)
+            if c.frame_tokens:
+                self.fnoise = dev(synth_inputs.flow_noise(5, ids, c.frame_tokens, c.frame_dim))
+                self.fout = torch.empty_like(self.fnoise)
         else:
             self.tok = torch.empty((n, c.n_action_tokens), dtype=torch.int32, device="cuda")
             self.act = torch.empty((n, c.n_action_tokens), dtype=torch.float32, device="cuda")
@@ -416,6 +423,9 @@ class Workload:
         self.pol.prefill(self.ids, images=self.img, lang_ids=self.lang)
 
     def head(self):
+        if self.c.frame_tokens:
+            self.pol.wam_denoise(self.ids, self.fnoise, self.noise, out_frames=self.fout, out_actions=self.out)
+            return self.n * self.c.chunk
         if self.c.exp_layers:
             self.pol.flow_denoise(self.ids, self.noise, out=self.out)
             return self.n * self.c.chunk
@@ -600,6 +610,10 @@ def main():
     if args.workload == "ragged-7b":
         desc = (f"ragged-7b: preset 3 (7B-class), pool of 128 language-only prefixes (T ~ U[200, 320]), "
                 f"{args.steps} decode calls of n ~ U[1, 128] envs")
+    elif c.frame_tokens:
+        desc = (f"{args.workload}: preset {preset}, {n} envs, prefix {c.max_seq} tokens, {c.layers}-layer "
+                f"d={c.d} backbone + {c.n_steps} Euler steps of the {c.exp_layers}-layer diffusion transformer over "
+                f"{c.frame_tokens} future-frame latents ({c.frame_dim} ch) + chunk {c.chunk}x{c.adim} per env")
     elif c.exp_layers:
         desc = (f"{args.workload}: preset {preset}, {n} envs, prefix {c.max_seq} tokens, {c.layers}-layer "
                 f"d={c.d} backbone + {c.n_steps} Euler steps of the {c.exp_layers}-layer expert, chunk {c.chunk}x{c.adim}")

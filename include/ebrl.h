@@ -75,6 +75,10 @@ typedef struct ebrl_config {
     int32_t max_seq;          /* longest prefix T_e accepted by ebrl_prefill */
     int64_t kv_budget_bytes;  /* KV pool size; 0 = enough for every env at max_seq */
     double init_std;          /* weight init N(0, init_std^2); presets use 0.02 */
+    /* world action model (Section 2.1): the expert also denoises frame_tokens
+       latent future-frame tokens of frame_dim channels per env jointly with
+       the action chunk (0 = actions only) */
+    int32_t frame_tokens, frame_dim;
 } ebrl_config;
 
 /* Observation batch for ebrl_prefill.  Env i's prefix is its image tokens
@@ -89,8 +93,10 @@ typedef struct ebrl_obs_batch {
     int32_t lang_stride;      /* row stride of lang_ids in elements (>= every lang_len) */
 } ebrl_obs_batch;
 
-/* Fill *out with preset 1..4 (1 tiny fp32 VLA, 2 small bf16 VLA, 3 7B-class
- * bf16 VLA with ViT, 4 flow-matching expert on a GQA backbone); capacity
+/* Fill *out with preset 1..5 (1 tiny fp32 VLA, 2 small bf16 VLA, 3 7B-class
+ * bf16 VLA with ViT, 4 flow-matching expert on a GQA backbone, 5 world
+ * action model: preset 4's backbone and expert denoising two future frames
+ * of 7 x 7 latent tokens (32 channels) with the action chunk); capacity
  * fields get the workload's batch size and prefix length.  Returns
  * EBRL_E_INVALID for any other preset. */
 int ebrl_config_preset(int32_t preset, ebrl_config* out);
@@ -143,9 +149,24 @@ int ebrl_decode_actions(ebrl_policy* p, const int32_t* env_ids, int32_t n, int32
  * backbone KV cache layer by layer plus its own chunk tokens.
  * noise: device float32 [n, chunk, adim]; out_actions: device float32
  * [n, chunk, adim] (may alias noise).  EBRL_E_UNSUPPORTED without an
- * expert, EBRL_E_STATE for an env with no prefix. */
+ * expert or for a world action model (frame_tokens > 0: use
+ * ebrl_wam_denoise), EBRL_E_STATE for an env with no prefix. */
 int ebrl_flow_denoise(ebrl_policy* p, const int32_t* env_ids, int32_t n, const float* noise,
                       float* out_actions);
+
+/* World-action-model denoising (Section 2.1: a diffusion transformer that
+ * jointly denoises latent future frames and the action chunk, each modality
+ * with its own decoder): the same Euler schedule as ebrl_flow_denoise over
+ * frame_tokens + chunk tokens per env -- frame latents at positions T_e ..
+ * T_e + frame_tokens - 1, then the actions -- that attend to each other
+ * without a mask and to the env's backbone cache.  Frame tokens enter
+ * through W_fin [exp_d, frame_dim] and leave through the final norm and
+ * W_fout [frame_dim, exp_d]; actions as in ebrl_flow_denoise.
+ * frame_noise / out_frames: device float32 [n, frame_tokens, frame_dim];
+ * action_noise / out_actions: device float32 [n, chunk, adim] (outputs may
+ * alias their noise).  EBRL_E_UNSUPPORTED unless frame_tokens > 0. */
+int ebrl_wam_denoise(ebrl_policy* p, const int32_t* env_ids, int32_t n, const float* frame_noise,
+                     const float* action_noise, float* out_frames, float* out_actions);
 
 /* Message describing the last failure on p (never NULL; "" if none).
  * With p == NULL: the last failure of ebrl_policy_create on this thread. */
@@ -177,7 +198,8 @@ int ebrl_read_state(ebrl_policy* p, int32_t what, int32_t env_id, int32_t layer,
  * (bf16 bit patterns when bf16 != 0, else float32).  Tensor ids:
  * 1 patch embedding, 2 language embedding, 3 action-token embedding,
  * 4 action logits, 5 ViT position embedding, 6 ViT projector, 7 expert
- * action-in, 8/9 expert time-MLP, 10 expert action-out; layer l of the
+ * action-in, 8/9 expert time-MLP, 10 expert action-out, 11 frame-latent
+ * in, 12 frame-latent out; layer l of the
  * decoder / ViT / expert uses base 1000 / 2000 / 3000 + 16 l plus
  * 0 q, 1 k, 2 v, 3 o, 4 gate, 5 up, 6 down. */
 int ebrl_generate_weight_host(uint64_t seed, uint32_t tensor_id, int64_t count, double std,

@@ -77,6 +77,8 @@ class Config:
     chunk: int = 0
     adim: int = 0
     n_steps: int = 0
+    frame_tokens: int = 0        # world action model: latent future-frame tokens per env
+    frame_dim: int = 0           # channels of a frame-latent token
     std: float = 0.02
     eps: float = 1e-6
     rope_base: float = 10000.0
@@ -114,11 +116,18 @@ PRESETS: Dict[int, Config] = {
               q_heads=16, kv_heads=8, head_dim=128, mlp=8192, vocab=32000, n_lang=12,
               action_logits=False, exp_layers=18, exp_d=1024, exp_heads=8, exp_mlp=4096,
               chunk=50, adim=7, n_steps=10),
+    # world action model: preset 4's backbone and expert, which also denoises
+    # two future frames of 7 x 7 latent tokens (32 channels each)
+    5: Config("wam-bf16", bf16=True, n_cams=3, img=224, patch=16, layers=18, d=2048,
+              q_heads=16, kv_heads=8, head_dim=128, mlp=8192, vocab=32000, n_lang=12,
+              action_logits=False, exp_layers=18, exp_d=1024, exp_heads=8, exp_mlp=4096,
+              chunk=50, adim=7, n_steps=10, frame_tokens=98, frame_dim=32),
 }
 
 # Tensor enumeration used to key the weight generator (counter word 2).
 TID_PATCH, TID_ELANG, TID_EACT, TID_WACT = 1, 2, 3, 4
 TID_VITPOS, TID_PROJ, TID_AIN, TID_T1, TID_T2, TID_AOUT = 5, 6, 7, 8, 9, 10
+TID_FIN, TID_FOUT = 11, 12
 STACK_BASE = {"dec": 1000, "vit": 2000, "exp": 3000}
 SLOT = {"q": 0, "k": 1, "v": 2, "o": 3, "gate": 4, "up": 5, "down": 6}
 
@@ -140,6 +149,9 @@ def tensor_shapes(cfg: Config) -> Dict[str, tuple]:
         s["W_t1"] = (TID_T1, (cfg.exp_d, cfg.exp_d))
         s["W_t2"] = (TID_T2, (cfg.exp_d, cfg.exp_d))
         s["W_aout"] = (TID_AOUT, (cfg.adim, cfg.exp_d))
+        if cfg.frame_tokens:
+            s["W_fin"] = (TID_FIN, (cfg.exp_d, cfg.frame_dim))
+            s["W_fout"] = (TID_FOUT, (cfg.frame_dim, cfg.exp_d))
 
     def stack(kind, n, d, hq, hkv, hd, mlp):
         for l in range(n):
@@ -598,6 +610,51 @@ class Policy:
 
         x = euler_integrate(np.asarray(noise, dtype=np.float64), vel, self.cfg.n_steps)
         return (x, v0[0]) if return_v0 else x
+
+
+    # world action model ------------------------------------------------------
+    def joint_velocity(self, st: PrefixState, xf: np.ndarray, xa: np.ndarray, tau: float):
+        """The diffusion transformer's velocity for one env's frame latents
+        xf [F, frame_dim] and action chunk xa [chunk, adim]: each modality
+        enters through its own input projection (plus the shared time
+        vector), all F + chunk tokens run through the expert blocks together
+        -- frames at positions T .. T+F-1, actions after them, no mask among
+        them, the backbone cache of the same layer as context -- and leave
+        through the final norm and each modality's own output projection."""
+        cfg = self.cfg
+        F = xf.shape[0]
+        t = self.time_vector(tau)[None, :]
+        h = np.concatenate([linear(xf, self.W("W_fin")) + t, linear(xa, self.W("W_ain")) + t], axis=0)
+        pos = st.T + np.arange(F + cfg.chunk)
+        ppos = np.arange(st.T)
+        for l in range(cfg.exp_layers):
+            h, _, _ = self.block(h, self.layer("exp", l), cfg.exp_heads, cfg.exp_heads,
+                                 cfg.head_dim, pos, st.k[l], st.v[l], ppos, causal=False)
+        y = rmsnorm(h, cfg.eps)
+        return linear(y[:F], self.W("W_fout")), linear(y[F:], self.W("W_aout"))
+
+    def wam_denoise(self, st: PrefixState, frame_noise: np.ndarray, action_noise: np.ndarray,
+                    return_v0: bool = False):
+        """Both modalities integrated by the same Euler schedule as the
+        action-only expert, from their noises at tau = 1."""
+        F = frame_noise.shape[0]
+        x0 = np.concatenate([np.asarray(frame_noise, dtype=np.float64).reshape(F, -1),
+                             np.asarray(action_noise, dtype=np.float64).reshape(self.cfg.chunk, -1)], axis=None)
+        nf = frame_noise.size
+        v0 = []
+
+        def vel(x, tau):
+            vf, va = self.joint_velocity(st, x[:nf].reshape(F, -1), x[nf:].reshape(self.cfg.chunk, -1), tau)
+            v = np.concatenate([vf.reshape(-1), va.reshape(-1)])
+            if not v0:
+                v0.append(v)
+            return v
+
+        x = euler_integrate(x0, vel, self.cfg.n_steps)
+        out = (x[:nf].reshape(frame_noise.shape), x[nf:].reshape(action_noise.shape))
+        if return_v0:
+            return out + (v0[0][nf:].reshape(action_noise.shape),)
+        return out
 
 
 def load_config(preset: int) -> Config:

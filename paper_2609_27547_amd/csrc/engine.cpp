@@ -67,6 +67,7 @@ struct ebrl_policy {
     void *w_pe = nullptr, *e_lang = nullptr, *e_act = nullptr, *w_act = nullptr;
     void *vit_pos = nullptr, *w_proj = nullptr;
     void *w_ain = nullptr, *w_t1 = nullptr, *w_t2 = nullptr, *w_aout = nullptr;
+    void *w_fin = nullptr, *w_fout = nullptr;   // world action model: frame latents in / out
     std::vector<LayerW> L_dec, L_vit, L_exp;
 
     // paged KV
@@ -108,6 +109,7 @@ struct ebrl_policy {
     size_t part_floats = 0;
     float* flow_x = nullptr;
     float* flow_v0 = nullptr;
+    float* flow_f = nullptr;   // frame latents being denoised
     std::vector<int> last_flow_ids;
 
     // per-call metadata
@@ -269,7 +271,7 @@ int upload_meta(ebrl_policy* p, const Meta& m, bool with_bt, int** dev) {
 // -------------------------------------------------------------- weights --
 
 enum { TID_PATCH = 1, TID_ELANG, TID_EACT, TID_WACT, TID_VITPOS, TID_PROJ, TID_AIN, TID_T1, TID_T2,
-       TID_AOUT };
+       TID_AOUT, TID_FIN, TID_FOUT };
 enum { SLOT_Q = 0, SLOT_K, SLOT_V, SLOT_O, SLOT_GATE, SLOT_UP, SLOT_DOWN };
 
 // Where a logical tensor lives on the device.
@@ -314,6 +316,8 @@ Placement placement(const ebrl_policy* p, uint32_t tid) {
     case TID_T1: plain(p->w_t1, c.exp_d, c.exp_d, c.exp_d); return pl;
     case TID_T2: plain(p->w_t2, c.exp_d, c.exp_d, c.exp_d); return pl;
     case TID_AOUT: plain(p->w_aout, c.adim, c.exp_d, c.exp_d); return pl;
+    case TID_FIN: plain(p->w_fin, c.exp_d, c.frame_dim, c.frame_dim); return pl;
+    case TID_FOUT: plain(p->w_fout, c.frame_dim, c.exp_d, c.exp_d); return pl;
     default: break;
     }
     const std::vector<LayerW>* layers = nullptr;
@@ -421,12 +425,15 @@ int validate(const ebrl_config& c, std::string& why) {
         if (c.exp_heads != c.kv_heads) return bad("expert heads must equal backbone kv heads");
         if (c.chunk < 1 || c.adim < 1 || c.n_steps < 1) return bad("flow chunk / steps");
     }
+    if (c.frame_tokens < 0 || (c.frame_tokens > 0 && (!c.exp_layers || c.frame_dim < 1)))
+        return bad("frame tokens need an expert and frame_dim >= 1");
     if (!c.action_logits && !c.exp_layers) return bad("no action head and no expert");
     if (c.max_envs < 1 || c.max_seq < 1) return bad("capacity");
     if (!(c.init_std > 0.0)) return bad("init_std");
     {
         // the bf16 attention kernels stage a sequence's block table in LDS
-        const int tail = std::max(c.action_logits ? c.n_action_tokens - 1 : 0, c.exp_layers ? c.chunk : 0);
+        const int tail =
+            std::max(c.action_logits ? c.n_action_tokens - 1 : 0, c.exp_layers ? c.chunk + c.frame_tokens : 0);
         const int blocks = (c.max_seq + tail + KV_BLOCK - 1) / KV_BLOCK;
         const int vit_blocks =
             c.n_cams ? (c.n_cams * (c.img / c.patch) * (c.img / c.patch) + KV_BLOCK - 1) / KV_BLOCK : 0;
@@ -603,6 +610,87 @@ int run_graph(ebrl_policy* p, const std::vector<uint64_t>& key, int classes, con
     return EBRL_OK;
 }
 
+// Flow-matching denoising of each env's token block -- frame_tokens
+// future-frame latents (world action model only), then the action chunk --
+// by the expert, attending to the env's backbone cache and, without a mask,
+// to the block itself; Euler steps on both modalities at once.
+int denoise(ebrl_policy* p, const int32_t* env_ids, int32_t n, const float* fnoise, const float* anoise,
+            float* fout, float* aout) {
+    const ebrl_config& c = p->cfg;
+    int rc;
+    if ((rc = check_ids(p, env_ids, n, true))) return rc;
+    if (n == 0) return EBRL_OK;
+    if (!anoise || !aout) return fail(p, EBRL_E_INVALID, "noise / out_actions is NULL");
+    const int F = c.frame_tokens, S = F + c.chunk;
+    const int rows = n * S, arows = n * c.chunk, frows = n * F;
+    std::vector<int> seq_env(env_ids, env_ids + n), q_off(n), q_len(n, S), q_pos0(n), kv_len(n),
+        row_seq(rows), row_pos(rows), tseq, tq0;
+    int maxkv = 0;
+    for (int i = 0; i < n; ++i) {
+        const int T = p->envs[env_ids[i]].T;
+        q_off[i] = i * S;
+        q_pos0[i] = T;
+        kv_len[i] = T + S;
+        maxkv = std::max(maxkv, kv_len[i]);
+        for (int j = 0; j < S; ++j) { row_seq[i * S + j] = i; row_pos[i * S + j] = T + j; }
+        for (int q0 = 0; q0 < S; q0 += 64) { tseq.push_back(i); tq0.push_back(q0); }
+    }
+    Meta m;
+    const size_t o_env = m.add(seq_env), o_off = m.add(q_off), o_len = m.add(q_len), o_pos0 = m.add(q_pos0),
+                 o_kvl = m.add(kv_len), o_rseq = m.add(row_seq), o_rpos = m.add(row_pos), o_tseq = m.add(tseq),
+                 o_tq0 = m.add(tq0);
+    int* md = nullptr;
+    if ((rc = upload_meta(p, m, false, &md))) return rc;
+    auto body = [&]() -> int {
+        // time-MLP outputs for the fixed tau schedule
+        prof_begin(p, EBRL_K_OTHER);
+        small_linear(p->bf16, p->temb, c.n_steps, c.exp_d, p->w_t1, c.exp_d, p->tmid, false, p->stream);
+        small_linear(p->bf16, p->tmid, c.n_steps, c.exp_d, p->w_t2, c.exp_d, p->tvec, true, p->stream);
+        copy_f32(anoise, p->flow_x, (size_t)arows * c.adim, p->stream);
+        if (F) copy_f32(fnoise, p->flow_f, (size_t)frows * c.frame_dim, p->stream);
+        prof_end(p, 0, 0);
+        for (int k = 0; k < c.n_steps; ++k) {
+            const float* tv = p->tvec + (size_t)k * c.exp_d;
+            prof_begin(p, EBRL_K_OTHER);
+            if (F) flow_in(p->bf16, p->flow_f, frows, c.frame_dim, p->w_fin, tv, c.exp_d, p->X, c.exp_d, F, S, 0,
+                           p->stream);
+            flow_in(p->bf16, p->flow_x, arows, c.adim, p->w_ain, tv, c.exp_d, p->X, c.exp_d, c.chunk, S, F,
+                    p->stream);
+            prof_end(p, 0, 0);
+            for (int l = 0; l < c.exp_layers; ++l) {
+                BlockCall b;
+                b.R = p->X; b.rows = rows; b.sd = &p->exp; b.w = &p->L_exp[l]; b.kv = dec_kv(p, l);
+                b.seq_env = md + o_env; b.row_seq = md + o_rseq; b.row_pos = md + o_rpos;
+                b.pre.seq_env = md + o_env; b.pre.q_off = md + o_off; b.pre.q_len = md + o_len;
+                b.pre.q_pos0 = md + o_pos0; b.pre.kv_len = md + o_kvl; b.pre.tile_seq = md + o_tseq;
+                b.pre.tile_q0 = md + o_tq0; b.pre.n_tiles = (int)tseq.size(); b.pre.causal = false;
+                b.pre.max_kv_len = maxkv;
+                b.attn_flop = 0;
+                for (int i = 0; i < n; ++i) b.attn_flop += 4.0 * c.head_dim * p->exp.hq * (double)S * kv_len[i];
+                int rc2 = run_block(p, b);
+                if (rc2) return rc2;
+            }
+            prof_begin(p, EBRL_K_OTHER);
+            if (F) flow_out(p->bf16, p->X, c.exp_d, frows, c.exp_d, p->w_fout, c.frame_dim, 1e-6f, (float)c.n_steps,
+                            p->flow_f, nullptr, F, S, 0, p->stream);
+            flow_out(p->bf16, p->X, c.exp_d, arows, c.exp_d, p->w_aout, c.adim, 1e-6f, (float)c.n_steps, p->flow_x,
+                     k == 0 ? p->flow_v0 : nullptr, c.chunk, S, F, p->stream);
+            prof_end(p, 0, 0);
+        }
+        copy_f32(p->flow_x, aout, (size_t)arows * c.adim, p->stream);
+        if (F) copy_f32(p->flow_f, fout, (size_t)frows * c.frame_dim, p->stream);
+        return check_launch(p);
+    };
+    const std::vector<uint64_t> key = {2, (uint64_t)n, (uint64_t)maxkv, (uint64_t)(uintptr_t)anoise,
+                                       (uint64_t)(uintptr_t)aout, (uint64_t)(uintptr_t)fnoise,
+                                       (uint64_t)(uintptr_t)fout};
+    const int inside = (1 << EBRL_K_GEMM) | (1 << EBRL_K_GEMM_SKINNY) | (1 << EBRL_K_ATTN_PREFILL) |
+                       (1 << EBRL_K_OTHER);
+    if ((rc = run_graph(p, key, inside, body))) return rc;
+    p->last_flow_ids.assign(env_ids, env_ids + n);
+    return check_launch(p);
+}
+
 }  // namespace
 
 // =================================================================== ABI ==
@@ -635,11 +723,13 @@ int ebrl_config_preset(int32_t preset, ebrl_config* out) {
         c.vocab = 32000; c.n_lang = 32; c.max_envs = 32; c.max_seq = 288;
         break;
     case 4:  // flow-matching expert on a GQA backbone
+    case 5:  // world action model: the same, also denoising latent future frames
         c.dtype = EBRL_DTYPE_BF16; c.n_cams = 3; c.img = 224; c.patch = 16;
         c.layers = 18; c.d = 2048; c.q_heads = 16; c.kv_heads = 8; c.head_dim = 128; c.mlp = 8192;
         c.vocab = 32000; c.n_lang = 12; c.action_logits = 0;
         c.exp_layers = 18; c.exp_d = 1024; c.exp_heads = 8; c.exp_mlp = 4096;
         c.chunk = 50; c.adim = 7; c.n_steps = 10; c.max_envs = 64; c.max_seq = 600;
+        if (preset == 5) { c.frame_tokens = 98; c.frame_dim = 32; }
         break;
     default:
         return EBRL_E_INVALID;
@@ -698,7 +788,7 @@ int ebrl_policy_create(const ebrl_config* config, uint64_t seed, ebrl_policy** o
     p->kpad = (pdim + 63) / 64 * 64;
     p->patches_per_env = c.n_cams ? c.n_cams * (c.img / c.patch) * (c.img / c.patch) : 0;
     p->n_img = p->patches_per_env;
-    p->tail = std::max(c.action_logits ? c.n_action_tokens - 1 : 0, c.exp_layers ? c.chunk : 0);
+    p->tail = std::max(c.action_logits ? c.n_action_tokens - 1 : 0, c.exp_layers ? c.chunk + c.frame_tokens : 0);
     p->bt_stride = (c.max_seq + p->tail + KV_BLOCK - 1) / KV_BLOCK;
     p->max_pos = c.max_seq + p->tail + 1;
 
@@ -721,6 +811,10 @@ int ebrl_policy_create(const ebrl_config* config, uint64_t seed, ebrl_policy** o
         if ((rc = dev_alloc(p, &p->w_t1, (size_t)c.exp_d * c.exp_d * p->esz))) return bail(rc);
         if ((rc = dev_alloc(p, &p->w_t2, (size_t)c.exp_d * c.exp_d * p->esz))) return bail(rc);
         if ((rc = dev_alloc(p, &p->w_aout, (size_t)c.adim * c.exp_d * p->esz))) return bail(rc);
+        if (c.frame_tokens) {
+            if ((rc = dev_alloc(p, &p->w_fin, (size_t)c.exp_d * c.frame_dim * p->esz))) return bail(rc);
+            if ((rc = dev_alloc(p, &p->w_fout, (size_t)c.frame_dim * c.exp_d * p->esz))) return bail(rc);
+        }
         if ((rc = alloc_stack(p, p->L_exp, p->exp))) return bail(rc);
     }
     if (c.n_cams && (rc = fill_buffer(p, {TID_PATCH}))) return bail(rc);
@@ -738,6 +832,9 @@ int ebrl_policy_create(const ebrl_config* config, uint64_t seed, ebrl_policy** o
     if (c.exp_layers) {
         for (uint32_t t : {TID_AIN, TID_T1, TID_T2, TID_AOUT})
             if ((rc = fill_buffer(p, {t}))) return bail(rc);
+        if (c.frame_tokens)
+            for (uint32_t t : {TID_FIN, TID_FOUT})
+                if ((rc = fill_buffer(p, {t}))) return bail(rc);
         if ((rc = fill_stack(p, 3000, c.exp_layers))) return bail(rc);
     }
 
@@ -795,7 +892,7 @@ int ebrl_policy_create(const ebrl_config* config, uint64_t seed, ebrl_policy** o
     // ---- activations
     const size_t pre_rows = (size_t)c.max_envs * c.max_seq;
     const size_t vit_rows = c.vit_layers ? (size_t)c.max_envs * p->patches_per_env : 0;
-    const size_t flow_rows = c.exp_layers ? (size_t)c.max_envs * c.chunk : 0;
+    const size_t flow_rows = c.exp_layers ? (size_t)c.max_envs * (c.chunk + c.frame_tokens) : 0;
     p->rows_cap = std::max({pre_rows, vit_rows, flow_rows, (size_t)c.max_envs});
     auto wmax = [&](auto f) {
         size_t m = f(p->dec);
@@ -844,8 +941,12 @@ int ebrl_policy_create(const ebrl_config* config, uint64_t seed, ebrl_policy** o
     p->part_floats = (size_t)c.max_envs * c.q_heads * max_splits * (c.head_dim + 2);
     if ((rc = dev_alloc_t(p, &p->part, p->part_floats))) return bail(rc);
     if (c.exp_layers) {
-        if ((rc = dev_alloc_t(p, &p->flow_x, flow_rows * c.adim))) return bail(rc);
-        if ((rc = dev_alloc_t(p, &p->flow_v0, flow_rows * c.adim))) return bail(rc);
+        const size_t act_rows = (size_t)c.max_envs * c.chunk;
+        if ((rc = dev_alloc_t(p, &p->flow_x, act_rows * c.adim))) return bail(rc);
+        if ((rc = dev_alloc_t(p, &p->flow_v0, act_rows * c.adim))) return bail(rc);
+        if (c.frame_tokens &&
+            (rc = dev_alloc_t(p, &p->flow_f, (size_t)c.max_envs * c.frame_tokens * c.frame_dim)))
+            return bail(rc);
     }
     // per-call metadata: generous bound on every call's int arrays
     p->meta_cap = 16 * (R + 64) + (size_t)c.max_envs * (32 + 2 * p->bt_stride) + p->bt_host.size() +
@@ -1130,70 +1231,20 @@ int ebrl_decode_actions(ebrl_policy* p, const int32_t* env_ids, int32_t n, int32
 int ebrl_flow_denoise(ebrl_policy* p, const int32_t* env_ids, int32_t n, const float* noise, float* out_actions) {
     int rc = check_ready(p);
     if (rc) return rc;
-    const ebrl_config& c = p->cfg;
-    if (!c.exp_layers) return fail(p, EBRL_E_UNSUPPORTED, "policy has no flow-matching expert");
-    if ((rc = check_ids(p, env_ids, n, true))) return rc;
-    if (n == 0) return EBRL_OK;
-    if (!noise || !out_actions) return fail(p, EBRL_E_INVALID, "noise / out_actions is NULL");
-    const int rows = n * c.chunk;
-    std::vector<int> seq_env(env_ids, env_ids + n), q_off(n), q_len(n, c.chunk), q_pos0(n), kv_len(n),
-        row_seq(rows), row_pos(rows), tseq, tq0;
-    int maxkv = 0;
-    for (int i = 0; i < n; ++i) {
-        const int T = p->envs[env_ids[i]].T;
-        q_off[i] = i * c.chunk;
-        q_pos0[i] = T;
-        kv_len[i] = T + c.chunk;
-        maxkv = std::max(maxkv, kv_len[i]);
-        for (int j = 0; j < c.chunk; ++j) { row_seq[i * c.chunk + j] = i; row_pos[i * c.chunk + j] = T + j; }
-        for (int q0 = 0; q0 < c.chunk; q0 += 64) { tseq.push_back(i); tq0.push_back(q0); }
-    }
-    Meta m;
-    const size_t o_env = m.add(seq_env), o_off = m.add(q_off), o_len = m.add(q_len), o_pos0 = m.add(q_pos0),
-                 o_kvl = m.add(kv_len), o_rseq = m.add(row_seq), o_rpos = m.add(row_pos), o_tseq = m.add(tseq),
-                 o_tq0 = m.add(tq0);
-    int* md = nullptr;
-    if ((rc = upload_meta(p, m, false, &md))) return rc;
-    auto body = [&]() -> int {
-        // time-MLP outputs for the fixed tau schedule
-        prof_begin(p, EBRL_K_OTHER);
-        small_linear(p->bf16, p->temb, c.n_steps, c.exp_d, p->w_t1, c.exp_d, p->tmid, false, p->stream);
-        small_linear(p->bf16, p->tmid, c.n_steps, c.exp_d, p->w_t2, c.exp_d, p->tvec, true, p->stream);
-        copy_f32(noise, p->flow_x, (size_t)rows * c.adim, p->stream);
-        prof_end(p, 0, 0);
-        for (int k = 0; k < c.n_steps; ++k) {
-            prof_begin(p, EBRL_K_OTHER);
-            flow_in(p->bf16, p->flow_x, rows, c.adim, p->w_ain, p->tvec + (size_t)k * c.exp_d, c.exp_d, p->X,
-                    c.exp_d, p->stream);
-            prof_end(p, 0, 0);
-            for (int l = 0; l < c.exp_layers; ++l) {
-                BlockCall b;
-                b.R = p->X; b.rows = rows; b.sd = &p->exp; b.w = &p->L_exp[l]; b.kv = dec_kv(p, l);
-                b.seq_env = md + o_env; b.row_seq = md + o_rseq; b.row_pos = md + o_rpos;
-                b.pre.seq_env = md + o_env; b.pre.q_off = md + o_off; b.pre.q_len = md + o_len;
-                b.pre.q_pos0 = md + o_pos0; b.pre.kv_len = md + o_kvl; b.pre.tile_seq = md + o_tseq;
-                b.pre.tile_q0 = md + o_tq0; b.pre.n_tiles = (int)tseq.size(); b.pre.causal = false;
-                b.pre.max_kv_len = maxkv;
-                b.attn_flop = 0;
-                for (int i = 0; i < n; ++i) b.attn_flop += 4.0 * c.head_dim * p->exp.hq * (double)c.chunk * kv_len[i];
-                int rc2 = run_block(p, b);
-                if (rc2) return rc2;
-            }
-            prof_begin(p, EBRL_K_OTHER);
-            flow_out(p->bf16, p->X, c.exp_d, rows, c.exp_d, p->w_aout, c.adim, 1e-6f, (float)c.n_steps, p->flow_x,
-                     k == 0 ? p->flow_v0 : nullptr, p->stream);
-            prof_end(p, 0, 0);
-        }
-        copy_f32(p->flow_x, out_actions, (size_t)rows * c.adim, p->stream);
-        return check_launch(p);
-    };
-    const std::vector<uint64_t> key = {2, (uint64_t)n, (uint64_t)maxkv, (uint64_t)(uintptr_t)noise,
-                                       (uint64_t)(uintptr_t)out_actions};
-    const int inside = (1 << EBRL_K_GEMM) | (1 << EBRL_K_GEMM_SKINNY) | (1 << EBRL_K_ATTN_PREFILL) |
-                       (1 << EBRL_K_OTHER);
-    if ((rc = run_graph(p, key, inside, body))) return rc;
-    p->last_flow_ids.assign(env_ids, env_ids + n);
-    return check_launch(p);
+    if (!p->cfg.exp_layers) return fail(p, EBRL_E_UNSUPPORTED, "policy has no flow-matching expert");
+    if (p->cfg.frame_tokens)
+        return fail(p, EBRL_E_UNSUPPORTED, "policy denoises future frames too: use ebrl_wam_denoise");
+    return denoise(p, env_ids, n, nullptr, noise, nullptr, out_actions);
+}
+
+int ebrl_wam_denoise(ebrl_policy* p, const int32_t* env_ids, int32_t n, const float* frame_noise,
+                     const float* action_noise, float* out_frames, float* out_actions) {
+    int rc = check_ready(p);
+    if (rc) return rc;
+    if (!p->cfg.exp_layers || !p->cfg.frame_tokens)
+        return fail(p, EBRL_E_UNSUPPORTED, "policy has no future-frame tokens");
+    if (n > 0 && (!frame_noise || !out_frames)) return fail(p, EBRL_E_INVALID, "frame_noise / out_frames is NULL");
+    return denoise(p, env_ids, n, frame_noise, action_noise, out_frames, out_actions);
 }
 
 int ebrl_read_state(ebrl_policy* p, int32_t what, int32_t env_id, int32_t layer, void* out, int64_t bytes) {

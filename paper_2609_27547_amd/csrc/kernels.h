@@ -170,11 +170,14 @@ void gather_last(const float* X, int ldx, const int* seq_env, const int* last_ro
 void small_linear(bool bf16, const float* in, int R, int K, const void* W, int N, float* out,
                   bool silu_input, hipStream_t s);
 
-// Flow-matching expert input and Euler update.
+// Flow-matching input projection (+ time vector) and output head + Euler
+// update of one denoised modality; its token r lives in row
+// (r / per_in) * per_out + off + r % per_in of H.
 void flow_in(bool bf16, const float* x, int rows, int adim, const void* W_ain, const float* tvec,
-             int d, float* H, int ldh, hipStream_t s);
+             int d, float* H, int ldh, int per_in, int per_out, int off, hipStream_t s);
 void flow_out(bool bf16, const float* H, int ldh, int rows, int d, const void* W_aout, int adim,
-              float eps, float n_steps, float* x, float* v_out, hipStream_t s);
+              float eps, float n_steps, float* x, float* v_out, int per_in, int per_out, int off,
+              hipStream_t s);
 
 // Element copy (device) with f32 -> f32.
 void copy_f32(const float* src, float* dst, size_t n, hipStream_t s);

@@ -446,41 +446,52 @@ void small_linear(bool bf16, const float* in, int R, int K, const void* W, int N
 }
 
 // ------------------------------------------------------------- flow --
+// The denoised tokens of one env sit in `per_out` consecutive rows of H; a
+// modality's token r (its rows numbered env by env, `per_in` per env) is
+// H row (r / per_in) * per_out + off + r % per_in.  Actions alone: per_in =
+// per_out = chunk, off = 0; the world-action model puts an env's future-frame
+// latents first and its action tokens after them.
+EBRL_DEV size_t flow_row(int r, int per_in, int per_out, int off) {
+    return (size_t)(r / per_in) * per_out + off + r % per_in;
+}
+
 template <typename T>
 __global__ __launch_bounds__(256) void flow_in_kernel(const float* x, int adim, const T* W_ain,
-                                                      const float* tvec, int d, float* H, int ldh)
+                                                      const float* tvec, int d, float* H, int ldh,
+                                                      int per_in, int per_out, int off)
 {
     const int r = blockIdx.x;
     const float* xr = x + (size_t)r * adim;
+    float* hr = H + flow_row(r, per_in, per_out, off) * ldh;
     for (int o = threadIdx.x; o < d; o += blockDim.x) {
         float acc = 0.f;
         for (int j = 0; j < adim; ++j) acc = fmaf(ld_elem<T>(W_ain + (size_t)o * adim + j), xr[j], acc);
-        H[(size_t)r * ldh + o] = acc + tvec[o];
+        hr[o] = acc + tvec[o];
     }
 }
 
 void flow_in(bool bf16, const float* x, int rows, int adim, const void* W_ain, const float* tvec,
-             int d, float* H, int ldh, hipStream_t s) {
+             int d, float* H, int ldh, int per_in, int per_out, int off, hipStream_t s) {
     if (rows <= 0) return;
     if (bf16)
         hipLaunchKernelGGL(flow_in_kernel<bf16_t>, dim3(rows), dim3(256), 0, s, x, adim,
-                           (const bf16_t*)W_ain, tvec, d, H, ldh);
+                           (const bf16_t*)W_ain, tvec, d, H, ldh, per_in, per_out, off);
     else
         hipLaunchKernelGGL(flow_in_kernel<float>, dim3(rows), dim3(256), 0, s, x, adim,
-                           (const float*)W_ain, tvec, d, H, ldh);
+                           (const float*)W_ain, tvec, d, H, ldh, per_in, per_out, off);
 }
 
 template <typename T>
 __global__ __launch_bounds__(256) void flow_out_kernel(const float* H, int ldh, int d, const T* W_aout,
                                                        int adim, float eps, float n_steps, float* x,
-                                                       float* v_out)
+                                                       float* v_out, int per_in, int per_out, int off)
 {
     extern __shared__ float sh[];
     float* hn = sh;          // [d]
     float* vv = sh + d;      // [adim]
     __shared__ float red[16];
     const int r = blockIdx.x;
-    const float* h = H + (size_t)r * ldh;
+    const float* h = H + flow_row(r, per_in, per_out, off) * ldh;
     const float rs = row_rstd(h, d, eps, red);
     for (int j = threadIdx.x; j < d; j += blockDim.x) hn[j] = h[j] * rs;
     __syncthreads();
@@ -492,8 +503,7 @@ __global__ __launch_bounds__(256) void flow_out_kernel(const float* H, int ldh, 
         if (lane == 0) vv[c] = dot;
     }
     __syncthreads();
-    if (threadIdx.x < adim) {
-        const int c = threadIdx.x;
+    for (int c = threadIdx.x; c < adim; c += blockDim.x) {
         const float v = vv[c];
         x[(size_t)r * adim + c] -= v / n_steps;
         if (v_out) v_out[(size_t)r * adim + c] = v;
@@ -501,15 +511,16 @@ __global__ __launch_bounds__(256) void flow_out_kernel(const float* H, int ldh, 
 }
 
 void flow_out(bool bf16, const float* H, int ldh, int rows, int d, const void* W_aout, int adim,
-              float eps, float n_steps, float* x, float* v_out, hipStream_t s) {
+              float eps, float n_steps, float* x, float* v_out, int per_in, int per_out, int off,
+              hipStream_t s) {
     if (rows <= 0) return;
     const size_t shm = (size_t)(d + adim) * sizeof(float);
     if (bf16)
         hipLaunchKernelGGL(flow_out_kernel<bf16_t>, dim3(rows), dim3(256), shm, s, H, ldh, d,
-                           (const bf16_t*)W_aout, adim, eps, n_steps, x, v_out);
+                           (const bf16_t*)W_aout, adim, eps, n_steps, x, v_out, per_in, per_out, off);
     else
         hipLaunchKernelGGL(flow_out_kernel<float>, dim3(rows), dim3(256), shm, s, H, ldh, d,
-                           (const float*)W_aout, adim, eps, n_steps, x, v_out);
+                           (const float*)W_aout, adim, eps, n_steps, x, v_out, per_in, per_out, off);
 }
 
 __global__ void copy_f32_kernel(const float* src, float* dst, size_t n) {

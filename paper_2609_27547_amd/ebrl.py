@@ -33,7 +33,8 @@ class Config(ctypes.Structure):
         "layers", "d", "q_heads", "kv_heads", "head_dim", "mlp", "vocab", "n_lang",
         "action_logits", "n_action_tokens", "n_bins",
         "exp_layers", "exp_d", "exp_heads", "exp_mlp", "chunk", "adim", "n_steps",
-        "max_envs", "max_seq")] + [("kv_budget_bytes", ctypes.c_int64), ("init_std", ctypes.c_double)]
+        "max_envs", "max_seq")] + [("kv_budget_bytes", ctypes.c_int64), ("init_std", ctypes.c_double),
+                                   ("frame_tokens", _I32), ("frame_dim", _I32)]
 
     def as_dict(self):
         return {n: getattr(self, n) for n, _ in self._fields_}
@@ -79,7 +80,7 @@ _LIB = None
 EXPORTED = [
     "ebrl_config_preset", "ebrl_policy_create", "ebrl_policy_destroy",
     "ebrl_stream_create_cu_masked", "ebrl_stream_destroy", "ebrl_policy_bind_stream",
-    "ebrl_prefill", "ebrl_decode_actions", "ebrl_flow_denoise", "ebrl_last_error",
+    "ebrl_prefill", "ebrl_decode_actions", "ebrl_flow_denoise", "ebrl_wam_denoise", "ebrl_last_error",
     "ebrl_read_state", "ebrl_generate_weight_host", "ebrl_read_weight", "ebrl_write_weight",
     "ebrl_profile_enable", "ebrl_profile_read", "ebrl_op_gemm", "ebrl_op_stream_read",
     "ebrl_alloc_solve", "ebrl_alloc_objective", "ebrl_alloc_monitor_create", "ebrl_alloc_monitor_observe",
@@ -110,6 +111,7 @@ def lib():
         "ebrl_prefill": (i32, [vp, ctypes.POINTER(ObsBatch), pI32, i32]),
         "ebrl_decode_actions": (i32, [vp, pI32, i32, vp, vp, vp]),
         "ebrl_flow_denoise": (i32, [vp, pI32, i32, vp, vp]),
+        "ebrl_wam_denoise": (i32, [vp, pI32, i32, vp, vp, vp, vp]),
         "ebrl_last_error": (ctypes.c_char_p, [vp]),
         "ebrl_read_state": (i32, [vp, i32, i32, i32, vp, i64]),
         "ebrl_generate_weight_host": (i32, [u64, u32, i64, ctypes.c_double, i32, vp]),
@@ -435,6 +437,18 @@ class Policy:
             out = torch.empty_like(noise)
         self._check(lib().ebrl_flow_denoise(self.h, pids, len(ids), _ptr(noise), _ptr(out)), "flow_denoise")
         return out
+
+    def wam_denoise(self, env_ids, frame_noise, action_noise, out_frames=None, out_actions=None):
+        """Joint denoising of future-frame latents and the action chunk."""
+        torch = self.torch
+        ids, pids = _ids(env_ids)
+        if out_frames is None:
+            out_frames = torch.empty_like(frame_noise)
+        if out_actions is None:
+            out_actions = torch.empty_like(action_noise)
+        self._check(lib().ebrl_wam_denoise(self.h, pids, len(ids), _ptr(frame_noise), _ptr(action_noise),
+                                           _ptr(out_frames), _ptr(out_actions)), "wam_denoise")
+        return out_frames, out_actions
 
     # inspection ------------------------------------------------------------
     def read_state(self, what: int, env_id: int, layer: int = 0) -> np.ndarray:

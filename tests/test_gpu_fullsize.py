@@ -139,6 +139,32 @@ def test_flow_expert_full_batch_sampled_env():
     pol.close()
 
 
+def test_world_action_model_full_batch_sampled_env():
+    # preset 5: 64 envs, 98 frame-latent tokens + 50 action tokens each
+    cfg = M.PRESETS[5]
+    ids = list(range(64))
+    img = synth_inputs.pixels(1005, ids, cfg.n_cams, cfg.img, cfg.img)
+    lang = synth_inputs.lang_ids(1005, ids, cfg.n_lang, cfg.vocab)
+    nf = synth_inputs.flow_noise(5, ids, cfg.frame_tokens, cfg.frame_dim)
+    na = synth_inputs.flow_noise(6, ids, cfg.chunk, cfg.adim)
+    pol = E.Policy(5, seed=0)
+    pol.prefill(ids, images=_dev(img), lang_ids=_dev(lang))
+    f, a = pol.wam_denoise(ids, _dev(nf), _dev(na))
+    torch.cuda.synchronize()
+    f, a = f.cpu().numpy(), a.cpu().numpy()
+    ref = M.Policy(cfg, seed=0)
+    e = 42
+    st = ref.prefill(img[e], lang[e])
+    xf, xa, v0 = ref.wam_denoise(st, nf[e], na[e], return_v0=True)
+    ef, ea = P.row_rel_err(f[e], xf), P.row_rel_err(a[e], xa)
+    ev = P.row_rel_err(pol.read_state(E.STATE_FLOW_V0, e), v0)
+    report("wam.frames", ef)
+    report("wam.actions", ea)
+    report("wam.v0", ev)
+    assert ef < P.TOL_BF16 and ea < P.TOL_BF16 and ev < P.TOL_BF16
+    pol.close()
+
+
 def balanced_mask(frac_quarters: int, n_cu: int = 256):
     """CU mask words selecting frac_quarters/4 of the CUs, 8-CU runs spread so
     that every XCD gets the same share whether the runtime numbers CUs XCD by

@@ -31,7 +31,8 @@ def _ebrl_config(o: M.Config, max_envs: int, max_seq: int = 0) -> "E.Config":
     c.dtype = E.DTYPE_BF16 if o.bf16 else E.DTYPE_FP32
     for f in ["n_cams", "img", "patch", "layers", "d", "q_heads", "kv_heads", "head_dim", "mlp", "vocab",
               "n_lang", "vit_layers", "vit_d", "vit_heads", "vit_mlp", "n_action_tokens", "n_bins",
-              "exp_layers", "exp_d", "exp_heads", "exp_mlp", "chunk", "adim", "n_steps"]:
+              "exp_layers", "exp_d", "exp_heads", "exp_mlp", "chunk", "adim", "n_steps", "frame_tokens",
+              "frame_dim"]:
         setattr(c, f, getattr(o, f))
     c.action_logits = int(o.action_logits)
     c.max_envs = max_envs
@@ -305,6 +306,47 @@ def test_tiny_flow_bf16_parity_and_zero_output_closed_form():
     out0 = pol.flow_denoise(ids, _dev(noise))
     torch.cuda.synchronize()
     assert np.array_equal(out0.cpu().numpy(), noise)
+    pol.close()
+
+
+# ----------------------------------------------------- tiny world action model --
+
+TINY_WAM = M.Config("tinywam", bf16=True, n_cams=1, img=32, patch=16, layers=2, d=128, q_heads=4,
+                    kv_heads=2, head_dim=64, mlp=256, vocab=100, n_lang=6, action_logits=False,
+                    exp_layers=2, exp_d=128, exp_heads=2, exp_mlp=256, chunk=50, adim=7, n_steps=10,
+                    frame_tokens=70, frame_dim=16)
+
+
+def test_tiny_wam_bf16_parity_and_closed_forms():
+    # 70 frame tokens + 50 action tokens: two query tiles per env, the
+    # second ragged
+    o = TINY_WAM
+    ids = [0, 2, 3]
+    img, lang = _obs(o, ids, 1005)
+    nf = synth_inputs.flow_noise(5, ids, o.frame_tokens, o.frame_dim)
+    na = synth_inputs.flow_noise(6, ids, o.chunk, o.adim)
+    pol = E.Policy(_ebrl_config(o, 4), seed=0)
+    pol.prefill(ids, images=_dev(img), lang_ids=_dev(lang))
+    f, a = pol.wam_denoise(ids, _dev(nf), _dev(na))
+    torch.cuda.synchronize()
+    f, a = f.cpu().numpy(), a.cpu().numpy()
+    ref = M.Policy(o, seed=0)
+    for i, e in enumerate(ids):
+        st = ref.prefill(img[i], lang[i])
+        xf, xa, v0 = ref.wam_denoise(st, nf[i], na[i], return_v0=True)
+        assert P.row_rel_err(pol.read_state(E.STATE_FLOW_V0, e), v0) < P.TOL_BF16
+        assert P.row_rel_err(f[i], xf) < P.TOL_BF16
+        assert P.row_rel_err(a[i], xa) < P.TOL_BF16
+    with pytest.raises(E.EbrlError) as ex:
+        pol.flow_denoise(ids, _dev(na))              # frames must be denoised too
+    assert ex.value.code == -5
+    # both output projections zero: the velocities vanish, outputs = noises bit for bit
+    for name in ("W_aout", "W_fout"):
+        tid, shape = M.tensor_shapes(o)[name]
+        pol.write_weight(tid, np.zeros(shape, np.uint16))
+    f0, a0 = pol.wam_denoise(ids, _dev(nf), _dev(na))
+    torch.cuda.synchronize()
+    assert np.array_equal(f0.cpu().numpy(), nf) and np.array_equal(a0.cpu().numpy(), na)
     pol.close()
 
 

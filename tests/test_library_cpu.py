@@ -34,14 +34,15 @@ def test_library_exports_every_declared_symbol():
     assert set(E.EXPORTED) == names
 
 
-@pytest.mark.parametrize("n", [1, 2, 3, 4])
+@pytest.mark.parametrize("n", [1, 2, 3, 4, 5])
 def test_presets_match_oracle_model_table(n):
     c = E.preset(n)
     o = M.PRESETS[n]
     assert c.dtype == (E.DTYPE_BF16 if o.bf16 else E.DTYPE_FP32)
     for f in ["n_cams", "img", "patch", "layers", "d", "q_heads", "kv_heads", "head_dim", "mlp",
               "vocab", "n_lang", "vit_layers", "vit_d", "vit_heads", "vit_mlp", "n_action_tokens",
-              "n_bins", "exp_layers", "exp_d", "exp_heads", "exp_mlp", "chunk", "adim", "n_steps"]:
+              "n_bins", "exp_layers", "exp_d", "exp_heads", "exp_mlp", "chunk", "adim", "n_steps",
+              "frame_tokens", "frame_dim"]:
         assert getattr(c, f) == getattr(o, f), f
     assert bool(c.action_logits) == o.action_logits
     assert c.max_seq == o.prefix_len

@@ -432,6 +432,83 @@ def test_flow_prefix_kv_is_read_per_layer():
     assert not np.allclose(pol.flow_denoise(st3, eps), base)
 
 
+def _tiny_wam_cfg(**kw):
+    return _tiny_flow_cfg(frame_tokens=4, frame_dim=6, **kw)
+
+
+def _wam_noise(cfg, seed=9):
+    nf = synth_inputs.flow_noise(seed, [0], cfg.frame_tokens, cfg.frame_dim)[0]
+    na = synth_inputs.flow_noise(seed + 1, [0], cfg.chunk, cfg.adim)[0]
+    return nf, na
+
+
+def test_wam_zero_output_projections_return_noise_exactly():
+    cfg = _tiny_wam_cfg()
+    pol = M.Policy(cfg, seed=0, overrides={"W_aout": np.zeros((cfg.adim, cfg.exp_d)),
+                                           "W_fout": np.zeros((cfg.frame_dim, cfg.exp_d))})
+    img, lang = _obs(cfg, [0])
+    st = pol.prefill(img[0], lang[0])
+    nf, na = _wam_noise(cfg)
+    f, a = pol.wam_denoise(st, nf, na)
+    assert np.array_equal(f, nf.astype(np.float64)) and np.array_equal(a, na.astype(np.float64))
+
+
+def test_wam_without_frame_tokens_is_the_action_expert():
+    # no frame tokens: the joint velocity is the action-only expert's
+    cfg = _tiny_wam_cfg()
+    pol = M.Policy(cfg, seed=0)
+    img, lang = _obs(cfg, [0])
+    st = pol.prefill(img[0], lang[0])
+    _, na = _wam_noise(cfg)
+    vf, va = pol.joint_velocity(st, np.zeros((0, cfg.frame_dim)), na.astype(np.float64), 0.7)
+    assert vf.shape == (0, cfg.frame_dim)
+    assert np.array_equal(va, pol.velocity(st, na.astype(np.float64), 0.7))
+
+
+def test_wam_actions_depend_on_frames_only_through_the_blocks():
+    # with the expert blocks zeroed every token sees only itself: the action
+    # chunk is the action-only expert's exactly, whatever the frame latents;
+    # with the blocks in place the frames steer the actions
+    cfg = _tiny_wam_cfg()
+    img, lang = _obs(cfg, [0])
+    nf, na = _wam_noise(cfg)
+    zero = M.Policy(cfg, seed=0, overrides=_zero_blocks(cfg, kinds=("exp",)))
+    st = zero.prefill(img[0], lang[0])
+    _, a0 = zero.wam_denoise(st, nf, na)
+    _, a1 = zero.wam_denoise(st, 3.0 * nf, na)
+    assert np.array_equal(a0, a1) and np.array_equal(a0, zero.flow_denoise(st, na))
+    pol = M.Policy(cfg, seed=0)
+    st = pol.prefill(img[0], lang[0])
+    _, b0 = pol.wam_denoise(st, nf, na)
+    _, b1 = pol.wam_denoise(st, 3.0 * nf, na)
+    assert not np.allclose(b0, b1)
+
+
+def test_wam_frames_zeroed_blocks_closed_form():
+    # zeroed blocks: frame token i's velocity is rmsnorm(x_i W_fin^T + t(tau)) W_fout^T
+    cfg = _tiny_wam_cfg()
+    pol = M.Policy(cfg, seed=0, overrides=_zero_blocks(cfg, kinds=("exp",)))
+    img, lang = _obs(cfg, [0])
+    st = pol.prefill(img[0], lang[0])
+    nf, na = _wam_noise(cfg)
+    f, _ = pol.wam_denoise(st, nf, na)
+    x = nf.astype(np.float64)
+    for k in range(10):
+        tau = 1 - k / 10
+        pre = pol.W("W_t1") @ M.time_embedding(tau, cfg.exp_d)
+        tv = pol.W("W_t2") @ (pre / (1 + np.exp(-pre)))
+        h = x @ pol.W("W_fin").T + tv
+        x = x - (M.rmsnorm(h) @ pol.W("W_fout").T) / 10
+    assert np.allclose(f, x, atol=1e-13)
+
+
+def test_wam_preset_shapes():
+    cfg = M.PRESETS[5]
+    sh = M.tensor_shapes(cfg)
+    assert sh["W_fin"] == (M.TID_FIN, (1024, 32)) and sh["W_fout"] == (M.TID_FOUT, (32, 1024))
+    assert cfg.frame_tokens + cfg.chunk == 148
+
+
 def test_tiny_preset_shapes_and_determinism():
     cfg = M.PRESETS[1]
     assert cfg.prefix_len == 24 and cfg.patch_dim == 768
