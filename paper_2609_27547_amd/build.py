@@ -22,6 +22,10 @@ HIP_FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
              "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
              "-Wno-unused-result", "-I", os.path.join(ROOT, "include")]
 HIP_SOURCES = ["gemm.hip", "attention.hip", "misc.hip", "engine.cpp"]
+# Per-source additions.  Attention: MFMA accumulators in VGPRs (gfx950 allows
+# either file), so the softmax rescale and the score reads need no
+# AGPR <-> VGPR copies every key tile.
+EXTRA_FLAGS = {"attention.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
 CXX_SOURCES = ["weights.cpp", "alloc.cpp", "sched.cpp"]
 
 
@@ -40,7 +44,7 @@ def build(verbose: bool = False) -> str:
     objs = []
     for src in HIP_SOURCES:
         obj = os.path.join(BUILD, src.replace(".", "_") + ".o")
-        cmd = [HIPCC] + HIP_FLAGS + ["-x", "hip", "-c", os.path.join(CSRC, src), "-o", obj]
+        cmd = [HIPCC] + HIP_FLAGS + EXTRA_FLAGS.get(src, []) + ["-x", "hip", "-c", os.path.join(CSRC, src), "-o", obj]
         jobs.append(cmd)
         objs.append(obj)
     for src in CXX_SOURCES:

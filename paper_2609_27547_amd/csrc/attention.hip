@@ -37,9 +37,13 @@ EBRL_DEV void attn_dma16(const void* g, uint32_t lds_addr) {
                  :: "v"(g), "s"(lds_addr) : "memory", "m0");
 }
 
-template <int HD>
-__global__ __launch_bounds__(256) void attn_prefill_bf16_kernel(AttnPrefillArgs a, float scale_log2)
+// One workgroup per (query tile of ATTN_Q_TILE rows, head): NW waves of 16
+// queries share every K/V tile staged in LDS, which each wave then skips if
+// none of its queries can see it.
+template <int HD, int NW>
+__global__ __launch_bounds__(64 * NW) void attn_prefill_bf16_kernel(AttnPrefillArgs a, float scale_log2)
 {
+    static_assert(16 * NW == ATTN_Q_TILE, "query tile");
     constexpr int KT = 64;                 // keys per tile
     constexpr int CPR = HD / 8;            // 16-byte chunks per K/V row
     constexpr int RPI = 64 / CPR;          // rows per DMA instruction
@@ -63,12 +67,17 @@ __global__ __launch_bounds__(256) void attn_prefill_bf16_kernel(AttnPrefillArgs 
     const int qpos = qpos0 + qi;
 
     int kv_end = kvlen;
-    if (a.causal) kv_end = min(kvlen, qpos0 + min(qt0 + 64, qlen));
+    if (a.causal) kv_end = min(kvlen, qpos0 + min(qt0 + ATTN_Q_TILE, qlen));
     // first key that some lane of this wave must mask: the end of the keys, or
     // (causal) the position of the wave's first query plus one
     const int mask_from = a.causal ? min(kvlen, qpos0 + qt0 + wave * 16 + 1) : kvlen;
+    // one past the last key this lane's query may see
+    const int key_lim = a.causal ? min(kvlen, qpos + 1) : kvlen;
+    // the last key any query of this wave may see (none: the wave idles)
+    const int wq0 = qt0 + wave * 16;
+    const int wave_keys = wq0 >= qlen ? 0 : (a.causal ? min(kvlen, qpos0 + min(wq0 + 16, qlen)) : kvlen);
     const int ntiles = (kv_end + KT - 1) / KT;
-    for (int b2 = tid; b2 < (kv_end + KV_BLOCK - 1) / KV_BLOCK; b2 += 256)
+    for (int b2 = tid; b2 < (kv_end + KV_BLOCK - 1) / KV_BLOCK; b2 += 64 * NW)
         s_bt[b2] = a.kv.block_table[(size_t)env * a.kv.bt_stride + b2];
 
     bf16x8 qb[HD / 32];
@@ -86,6 +95,7 @@ __global__ __launch_bounds__(256) void attn_prefill_bf16_kernel(AttnPrefillArgs 
     // DMA of key tile `it`: row q of the tile = key k0 + q, its 16-byte chunk
     // c stored at chunk position q * CPR + (c ^ (q & 7)); the waves split the
     // tile's 64 / RPI instructions for K and the same for V.
+    static_assert((KT / RPI) % NW == 0, "DMA split");
     const size_t blk_elems = (size_t)2 * hkv * KV_BLOCK * HD;
     const bf16_t* kbase = (const bf16_t*)a.kv.base + (size_t)kvh * KV_BLOCK * HD;
     const size_t voff = (size_t)hkv * KV_BLOCK * HD;
@@ -95,8 +105,8 @@ __global__ __launch_bounds__(256) void attn_prefill_bf16_kernel(AttnPrefillArgs 
         constexpr int NI = KT / RPI;             // instructions per operand
         const int row_in = lane / CPR, cpos = lane % CPR;
 #pragma unroll
-        for (int u = 0; u < NI / 4; ++u) {
-            const int ins = wave * (NI / 4) + u;
+        for (int u = 0; u < NI / NW; ++u) {
+            const int ins = wave * (NI / NW) + u;
             const int q = ins * RPI + row_in;
             const int key = min(it * KT + q, kv_end - 1);
             const int c = cpos ^ (q & 7);
@@ -122,6 +132,9 @@ __global__ __launch_bounds__(256) void attn_prefill_bf16_kernel(AttnPrefillArgs 
         const bf16_t* tk = sK[it & 1];
         const bf16_t* tv = sV[it & 1];
         const int k0 = it * KT;
+        // no query of this wave sees a key of this tile: nothing to add
+        // (processing it would leave m, l and acc as they are)
+        if (k0 >= wave_keys) continue;
 
         // S^T tiles: lane holds key 16kt + 4g + v for query r
         f32x4 s[4];
@@ -136,16 +149,20 @@ __global__ __launch_bounds__(256) void attn_prefill_bf16_kernel(AttnPrefillArgs 
                 s[kt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka, qb[ks], s[kt], 0, 0, 0);
             }
         }
+        // Row maximum of the raw scores: the scale is positive, so it
+        // commutes with the maximum and is applied once, inside the
+        // exponent's fused multiply-add.  Masked scores become -inf.
         float tmax = -INFINITY;
         if (mask_from <= k0 + KT - 1) {
-            // tile reaches past the keys or past a query of this wave
+            // tile reaches past the keys or past a query of this wave: key
+            // k0 + 16 kt + 4 g + v is visible to this lane's query iff
+            // 16 kt + v < lim
+            const int lim = key_lim - k0 - 4 * g;
 #pragma unroll
             for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
                 for (int v = 0; v < 4; ++v) {
-                    const int kidx = k0 + kt * 16 + 4 * g + v;
-                    const bool ok = kidx < kvlen && (!a.causal || kidx <= qpos);
-                    const float val = ok ? s[kt][v] * scale_log2 : -INFINITY;
+                    const float val = kt * 16 + v < lim ? s[kt][v] : -INFINITY;
                     s[kt][v] = val;
                     tmax = fmaxf(tmax, val);
                 }
@@ -153,10 +170,7 @@ __global__ __launch_bounds__(256) void attn_prefill_bf16_kernel(AttnPrefillArgs 
 #pragma unroll
             for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
-                for (int v = 0; v < 4; ++v) {
-                    s[kt][v] *= scale_log2;
-                    tmax = fmaxf(tmax, s[kt][v]);
-                }
+                for (int v = 0; v < 4; ++v) tmax = fmaxf(tmax, s[kt][v]);
         }
         tmax = fmaxf(tmax, swz_xor16_f(tmax));
         tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
@@ -164,7 +178,7 @@ __global__ __launch_bounds__(256) void attn_prefill_bf16_kernel(AttnPrefillArgs 
         // rescaling by alpha is then a power of two, which commutes with the
         // bf16 rounding of P, so P is rounded as 2^(x - ceil(row max)) no
         // matter how the keys are split into tiles.
-        const float m_new = fmaxf(m_i, ceilf(tmax));
+        const float m_new = fmaxf(m_i, ceilf(tmax * scale_log2));
         const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
         const float alpha = (m_i == -INFINITY) ? 0.f : ldexpf(1.0f, (int)(m_i - m_use));
         float psum = 0.f;
@@ -172,7 +186,7 @@ __global__ __launch_bounds__(256) void attn_prefill_bf16_kernel(AttnPrefillArgs 
         for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
             for (int v = 0; v < 4; ++v) {
-                const float p = fast_exp2(s[kt][v] - m_use);
+                const float p = fast_exp2(fmaf(s[kt][v], scale_log2, -m_use));
                 s[kt][v] = p;
                 psum += p;
             }
@@ -234,7 +248,7 @@ __global__ __launch_bounds__(256) void attn_prefill_bf16_kernel(AttnPrefillArgs 
 }
 
 // ---------------------------------------------------------- fp32 prefill --
-// grid (tile, head, 64 rows of the tile); one wave per query row.
+// grid (tile, head, ATTN_Q_TILE rows of the tile); one wave per query row.
 __global__ __launch_bounds__(64) void attn_prefill_f32_kernel(AttnPrefillArgs a, float scale)
 {
     extern __shared__ float sh[];
@@ -295,11 +309,12 @@ void attn_prefill(const AttnPrefillArgs& a, hipStream_t s) {
         if (a.kv.bt_stride > ATTN_BT_MAX) return;   // rejected by the caller (capacity check)
         const float scale_log2 = 1.4426950408889634f / sqrtf((float)hd);
         dim3 grid(a.n_tiles, a.q_heads);
-        if (hd == 64) hipLaunchKernelGGL(attn_prefill_bf16_kernel<64>, grid, dim3(256), 0, s, a, scale_log2);
-        else hipLaunchKernelGGL(attn_prefill_bf16_kernel<128>, grid, dim3(256), 0, s, a, scale_log2);
+        constexpr int NW = ATTN_Q_TILE / 16;
+        if (hd == 64) hipLaunchKernelGGL((attn_prefill_bf16_kernel<64, NW>), grid, dim3(64 * NW), 0, s, a, scale_log2);
+        else hipLaunchKernelGGL((attn_prefill_bf16_kernel<128, NW>), grid, dim3(64 * NW), 0, s, a, scale_log2);
     } else {
         const float scale = 1.0f / sqrtf((float)hd);
-        dim3 grid(a.n_tiles, a.q_heads, 64);
+        dim3 grid(a.n_tiles, a.q_heads, ATTN_Q_TILE);
         const size_t shm = (size_t)(hd + a.max_kv_len) * sizeof(float);
         hipLaunchKernelGGL(attn_prefill_f32_kernel, grid, dim3(64), shm, s, a, scale);
     }

@@ -633,7 +633,7 @@ int denoise(ebrl_policy* p, const int32_t* env_ids, int32_t n, const float* fnoi
         kv_len[i] = T + S;
         maxkv = std::max(maxkv, kv_len[i]);
         for (int j = 0; j < S; ++j) { row_seq[i * S + j] = i; row_pos[i * S + j] = T + j; }
-        for (int q0 = 0; q0 < S; q0 += 64) { tseq.push_back(i); tq0.push_back(q0); }
+        for (int q0 = 0; q0 < S; q0 += ATTN_Q_TILE) { tseq.push_back(i); tq0.push_back(q0); }
     }
     Meta m;
     const size_t o_env = m.add(seq_env), o_off = m.add(q_off), o_len = m.add(q_len), o_pos0 = m.add(q_pos0),
@@ -1057,7 +1057,7 @@ int ebrl_prefill(ebrl_policy* p, const ebrl_obs_batch* obs, const int32_t* env_i
         for (int t = 0; t < T[i]; ++t) { row_seq[tok_off[i] + t] = i; row_pos[tok_off[i] + t] = t; }
     std::vector<std::pair<int, int>> tiles;
     for (int i = 0; i < n; ++i)
-        for (int q0 = 0; q0 < T[i]; q0 += 64) tiles.push_back({i, q0});
+        for (int q0 = 0; q0 < T[i]; q0 += ATTN_Q_TILE) tiles.push_back({i, q0});
     // causal tiles late in a sequence see the most keys: dispatch them first
     std::stable_sort(tiles.begin(), tiles.end(),
                      [](const std::pair<int, int>& x, const std::pair<int, int>& y) { return x.second > y.second; });
@@ -1078,7 +1078,7 @@ int ebrl_prefill(ebrl_policy* p, const ebrl_obs_batch* obs, const int32_t* env_i
         for (int i = 0; i < n; ++i)
             for (int t = 0; t < pv; ++t) { v_rowseq.push_back(i); v_rowpos.push_back(t); }
         for (int i = 0; i < n; ++i)
-            for (int q0 = 0; q0 < pv; q0 += 64) { v_tseq.push_back(i); v_tq0.push_back(q0); }
+            for (int q0 = 0; q0 < pv; q0 += ATTN_Q_TILE) { v_tseq.push_back(i); v_tq0.push_back(q0); }
     }
     Meta m;
     const size_t o_env = m.add(seq_env), o_off = m.add(tok_off), o_len = m.add(T), o_pos0 = m.add(q_pos0),

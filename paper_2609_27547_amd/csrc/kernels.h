@@ -64,8 +64,9 @@ struct PagedKV {
     int kv_heads = 0, head_dim = 0;
 };
 
-// Flash attention over query tiles of 64 rows.  Tile t covers rows
-// [tile_q0[t], +64) of sequence tile_seq[t].
+// Flash attention over query tiles of ATTN_Q_TILE rows.  Tile t covers rows
+// [tile_q0[t], +ATTN_Q_TILE) of sequence tile_seq[t].
+constexpr int ATTN_Q_TILE = 64;
 struct AttnPrefillArgs {
     bool bf16 = true;
     const void* Q = nullptr; int ldq = 0;  // [rows, q_heads*hd]
