@@ -3,7 +3,7 @@
 Simulator workers are stood in for by a table of step durations (the
 paper's simulators are out of scope); the generation stage is a callable
 that takes a group's env ids and returns how long generating its next chunk
-took -- on a GPU machine, the time of the real prefill + action-head calls for
+took -- with a GPU, the time of the real prefill + action-head calls for
 that ragged group.  The event loop keeps one generation stage (groups served
 in the order they finished) and `cores` CPU cores; after every event, each
 free core asks the scheduler for work (Algorithm 2, or the fixed binding it
