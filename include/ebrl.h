@@ -68,7 +68,7 @@ typedef struct ebrl_config {
     int32_t layers, d, q_heads, kv_heads, head_dim, mlp, vocab, n_lang;
     /* autoregressive action head (action_logits = 0: none) */
     int32_t action_logits, n_action_tokens, n_bins;
-    /* flow-matching action expert (exp_layers = 0: none) */
+    /* flow-matching action expert (exp_layers = 0: none); adim <= 64 */
     int32_t exp_layers, exp_d, exp_heads, exp_mlp, chunk, adim, n_steps;
     /* capacity */
     int32_t max_envs;         /* env ids live in [0, max_envs); also max n per call */
@@ -77,7 +77,7 @@ typedef struct ebrl_config {
     double init_std;          /* weight init N(0, init_std^2); presets use 0.02 */
     /* world action model (Section 2.1): the expert also denoises frame_tokens
        latent future-frame tokens of frame_dim channels per env jointly with
-       the action chunk (0 = actions only) */
+       the action chunk (0 = actions only); frame_dim <= 64 */
     int32_t frame_tokens, frame_dim;
 } ebrl_config;
 

@@ -423,10 +423,10 @@ int validate(const ebrl_config& c, std::string& why) {
     if (c.exp_layers) {
         if (c.exp_d < 64 || c.exp_d % 64 || c.exp_mlp % 16 || c.exp_mlp < 16) return bad("expert dims");
         if (c.exp_heads != c.kv_heads) return bad("expert heads must equal backbone kv heads");
-        if (c.chunk < 1 || c.adim < 1 || c.n_steps < 1) return bad("flow chunk / steps");
+        if (c.chunk < 1 || c.adim < 1 || c.adim > 64 || c.n_steps < 1) return bad("flow chunk / action dims / steps");
     }
-    if (c.frame_tokens < 0 || (c.frame_tokens > 0 && (!c.exp_layers || c.frame_dim < 1)))
-        return bad("frame tokens need an expert and frame_dim >= 1");
+    if (c.frame_tokens < 0 || (c.frame_tokens > 0 && (!c.exp_layers || c.frame_dim < 1 || c.frame_dim > 64)))
+        return bad("frame tokens need an expert and 1 <= frame_dim <= 64");
     if (!c.action_logits && !c.exp_layers) return bad("no action head and no expert");
     if (c.max_envs < 1 || c.max_seq < 1) return bad("capacity");
     if (!(c.init_std > 0.0)) return bad("init_std");

@@ -4,6 +4,8 @@
 // update.  All reductions run in a fixed order (deterministic results).
 #include <math.h>
 
+#include <type_traits>
+
 #include "kernels.h"
 
 namespace ebrl {
@@ -417,32 +419,40 @@ void gather_last(const float* X, int ldx, const int* seq_env, const int* last_ro
 }
 
 // ------------------------------------------------------- small linear --
+// One wave per output column n, for all R input rows: the lanes read W's row
+// n and each input row in coalesced 64-element strides, then sum across the
+// wave (a fixed butterfly).
 template <typename T>
-__global__ void small_linear_kernel(const float* in, int R, int K, const T* W, int N, float* out,
-                                    int silu_input)
+__global__ __launch_bounds__(256) void small_linear_kernel(const float* in, int R, int K, const T* W, int N,
+                                                           float* out, int silu_input)
 {
-    const int idx = blockIdx.x * blockDim.x + threadIdx.x;
-    if (idx >= R * N) return;
-    const int r = idx / N, n = idx - r * N;
-    float acc = 0.f;
-    for (int k = 0; k < K; ++k) {
-        float v = in[(size_t)r * K + k];
-        if (silu_input) v = v / (1.0f + expf(-v));
-        acc = fmaf(v, ld_elem<T>(W + (size_t)n * K + k), acc);
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const int n = blockIdx.x * 4 + wave;
+    if (n >= N) return;
+    const T* w = W + (size_t)n * K;
+    for (int r = 0; r < R; ++r) {
+        const float* x = in + (size_t)r * K;
+        float acc = 0.f;
+        for (int k = lane; k < K; k += 64) {
+            float v = x[k];
+            if (silu_input) v = v / (1.0f + expf(-v));
+            acc = fmaf(v, ld_elem<T>(w + k), acc);
+        }
+        acc = wave_sum(acc);
+        if (lane == 0) out[(size_t)r * N + n] = acc;
     }
-    out[idx] = acc;
 }
 
 void small_linear(bool bf16, const float* in, int R, int K, const void* W, int N, float* out,
                   bool silu_input, hipStream_t s) {
-    const int total = R * N;
-    if (total <= 0) return;
+    if (R <= 0 || N <= 0) return;
+    const dim3 grid((N + 3) / 4);
     if (bf16)
-        hipLaunchKernelGGL(small_linear_kernel<bf16_t>, dim3((total + 255) / 256), dim3(256), 0, s, in,
-                           R, K, (const bf16_t*)W, N, out, (int)silu_input);
+        hipLaunchKernelGGL(small_linear_kernel<bf16_t>, grid, dim3(256), 0, s, in, R, K, (const bf16_t*)W, N,
+                           out, (int)silu_input);
     else
-        hipLaunchKernelGGL(small_linear_kernel<float>, dim3((total + 255) / 256), dim3(256), 0, s, in,
-                           R, K, (const float*)W, N, out, (int)silu_input);
+        hipLaunchKernelGGL(small_linear_kernel<float>, grid, dim3(256), 0, s, in, R, K, (const float*)W, N, out,
+                           (int)silu_input);
 }
 
 // ------------------------------------------------------------- flow --
@@ -455,30 +465,53 @@ EBRL_DEV size_t flow_row(int r, int per_in, int per_out, int off) {
     return (size_t)(r / per_in) * per_out + off + r % per_in;
 }
 
-template <typename T>
-__global__ __launch_bounds__(256) void flow_in_kernel(const float* x, int adim, const T* W_ain,
+// A workgroup projects FLOW_IN_ROWS tokens: their inputs sit in LDS and each
+// thread keeps one output's weight row in registers while it walks the rows,
+// so the weights are read once per workgroup instead of once per token.  Each
+// output is summed over the input channels in channel order.
+constexpr int FLOW_IN_ROWS = 64;
+template <typename T, int AMAX>
+__global__ __launch_bounds__(256) void flow_in_kernel(const float* x, int rows, int adim, const T* W_ain,
                                                       const float* tvec, int d, float* H, int ldh,
                                                       int per_in, int per_out, int off)
 {
-    const int r = blockIdx.x;
-    const float* xr = x + (size_t)r * adim;
-    float* hr = H + flow_row(r, per_in, per_out, off) * ldh;
+    __shared__ float sx[FLOW_IN_ROWS * AMAX];
+    const int r0 = blockIdx.x * FLOW_IN_ROWS;
+    const int nr = min(FLOW_IN_ROWS, rows - r0);
+    for (int i = threadIdx.x; i < nr * adim; i += blockDim.x) sx[i] = x[(size_t)r0 * adim + i];
+    __syncthreads();
     for (int o = threadIdx.x; o < d; o += blockDim.x) {
-        float acc = 0.f;
-        for (int j = 0; j < adim; ++j) acc = fmaf(ld_elem<T>(W_ain + (size_t)o * adim + j), xr[j], acc);
-        hr[o] = acc + tvec[o];
+        float w[AMAX];
+#pragma unroll
+        for (int j = 0; j < AMAX; ++j) w[j] = j < adim ? ld_elem<T>(W_ain + (size_t)o * adim + j) : 0.f;
+        const float t = tvec[o];
+        for (int q = 0; q < nr; ++q) {
+            const float* xr = sx + q * adim;
+            float acc = 0.f;
+#pragma unroll
+            for (int j = 0; j < AMAX; ++j)
+                if (j < adim) acc = fmaf(w[j], xr[j], acc);
+            H[flow_row(r0 + q, per_in, per_out, off) * ldh + o] = acc + t;
+        }
     }
 }
 
 void flow_in(bool bf16, const float* x, int rows, int adim, const void* W_ain, const float* tvec,
              int d, float* H, int ldh, int per_in, int per_out, int off, hipStream_t s) {
     if (rows <= 0) return;
-    if (bf16)
-        hipLaunchKernelGGL(flow_in_kernel<bf16_t>, dim3(rows), dim3(256), 0, s, x, adim,
-                           (const bf16_t*)W_ain, tvec, d, H, ldh, per_in, per_out, off);
-    else
-        hipLaunchKernelGGL(flow_in_kernel<float>, dim3(rows), dim3(256), 0, s, x, adim,
-                           (const float*)W_ain, tvec, d, H, ldh, per_in, per_out, off);
+    const dim3 grid((rows + FLOW_IN_ROWS - 1) / FLOW_IN_ROWS);
+    auto go = [&](auto amax) {
+        constexpr int AM = decltype(amax)::value;
+        if (bf16)
+            hipLaunchKernelGGL((flow_in_kernel<bf16_t, AM>), grid, dim3(256), 0, s, x, rows, adim,
+                               (const bf16_t*)W_ain, tvec, d, H, ldh, per_in, per_out, off);
+        else
+            hipLaunchKernelGGL((flow_in_kernel<float, AM>), grid, dim3(256), 0, s, x, rows, adim,
+                               (const float*)W_ain, tvec, d, H, ldh, per_in, per_out, off);
+    };
+    if (adim <= 8) go(std::integral_constant<int, 8>{});
+    else if (adim <= 32) go(std::integral_constant<int, 32>{});
+    else go(std::integral_constant<int, 64>{});   // adim <= 64 (checked at policy creation)
 }
 
 template <typename T>
