@@ -313,15 +313,24 @@ EBRL_DEV void dma16_to_lds_nt(const void* g, uint32_t lds_addr) {
 template <int ROWS, int NW>
 EBRL_DEV void load_tile_lds(const bf16_t* __restrict__ G, int ld, int row0_g, int rows_valid, int k0,
                             bf16_t* lds_tile, int wave, int lane) {
-    // each of the NW waves fills ROWS/NW rows, 8 rows per instruction
-#pragma unroll
-    for (int j = 0; j < ROWS / (8 * NW); ++j) {
-        const int r0 = wave * (ROWS / NW) + j * 8;
+    auto group = [&](int r0) {   // rows r0 .. r0+7, one instruction
         const int row = r0 + (lane >> 3);
         const int c = (lane & 7) ^ (row & 7);
         const int gr = min(row0_g + row, rows_valid - 1);
         const bf16_t* src = G + (size_t)gr * ld + k0 + c * 8;
         __builtin_amdgcn_global_load_lds((const void*)src, (lds_ptr_t)(lds_tile + r0 * 64), 16, 0, 0);
+    };
+    if constexpr (ROWS % (8 * NW) == 0) {
+        // each of the NW waves fills ROWS/NW consecutive rows
+#pragma unroll
+        for (int j = 0; j < ROWS / (8 * NW); ++j) group(wave * (ROWS / NW) + j * 8);
+    } else {
+        // 8-row groups dealt round-robin over the waves
+#pragma unroll
+        for (int j = 0; j < (ROWS / 8 + NW - 1) / NW; ++j) {
+            const int gi = wave + j * NW;
+            if (gi < ROWS / 8) group(gi * 8);
+        }
     }
 }
 
@@ -869,6 +878,31 @@ struct GemmPlan {
 // summation order; the split count (decode only) is a function of (N, K).
 constexpr int SPLIT_MAX_M = 256;
 
+// Macro tile of the large-M kernel: 256 x 256 (16 waves), 192 x 256 (12
+// waves) or 128 x 128 (4 waves, two workgroups per CU).  Each is priced as
+// the number of rounds its tiles take over the 256 CUs times one round's
+// work per CU, divided by the variant's throughput relative to 256 x 256
+// (measured: 0.85 and 0.8); the cheapest wins, ties to the larger tile.  The
+// smaller tiles pay off where 256 x 256 tiles leave most of a last round
+// idle (e.g. 576 tiles = 2.25 rounds).  Every variant runs the same K loop,
+// so an element's summation order does not depend on the choice.
+static void big_tile(int M, int N, int& bm, int& bn) {
+    constexpr int CUS = 256;
+    struct V { int bm, bn, per_cu; double rel; } vs[] = {{256, 256, 1, 1.0}, {192, 256, 1, 0.85}, {128, 128, 2, 0.8}};
+    double best = 0;
+    for (int i = 0; i < 3; ++i) {
+        const V& v = vs[i];
+        const long tiles = (long)((M + v.bm - 1) / v.bm) * ((N + v.bn - 1) / v.bn);
+        const long rounds = (tiles + (long)CUS * v.per_cu - 1) / ((long)CUS * v.per_cu);
+        const double cost = rounds * (double)v.bm * v.bn * v.per_cu / (65536.0 * v.rel);
+        if (i == 0 || cost < best * 0.999) {
+            best = cost;
+            bm = v.bm;
+            bn = v.bn;
+        }
+    }
+}
+
 static GemmPlan plan_gemm(bool bf16, int M, int N, int K, size_t ws_floats, bool split_ok) {
     GemmPlan p;
     p.big = false;
@@ -910,8 +944,7 @@ static GemmPlan plan_gemm(bool bf16, int M, int N, int K, size_t ws_floats, bool
     }
     if (bf16 && !split_ok && M >= 256 && K % 64 == 0) {
         p.big = true;
-        p.bm = 256;
-        p.bn = 256;
+        big_tile(M, N, p.bm, p.bn);
         return p;
     }
     if (!bf16) p.bm = 64;
@@ -940,19 +973,17 @@ template <bool PAIRED, class Epi>
 static void launch_bf16(const GemmArgs& a, const GemmPlan& p, Epi epi, hipStream_t s) {
     const bool split = p.splits > 1;
     if (p.big) {
-        // 256 x 256 tiles, or 128 x 128 (4 waves, two workgroups per CU)
-        // when the large tiles would fill less than half the chip; the K
-        // order of every sum is the same either way
-        const long t256 = (long)((a.M + 255) / 256) * ((a.N + 255) / 256);
-        if (t256 >= 128) {
-            dim3 grid((unsigned)t256, 1);
+        const long tiles = (long)((a.M + p.bm - 1) / p.bm) * ((a.N + p.bn - 1) / p.bn);
+        dim3 grid((unsigned)tiles, 1);
+        if (p.bm == 256)
             hipLaunchKernelGGL((gemm_bf16_big_kernel<256, 256, 4, 4, PAIRED, false, Epi>), grid, dim3(1024), 0, s,
                                (const bf16_t*)a.A, a.lda, (const bf16_t*)a.B, a.ldb, a.M, a.N, a.K, a.K, a.ws, epi);
-        } else {
-            dim3 grid(((a.M + 127) / 128) * ((a.N + 127) / 128), 1);
+        else if (p.bm == 192)
+            hipLaunchKernelGGL((gemm_bf16_big_kernel<192, 256, 3, 4, PAIRED, false, Epi>), grid, dim3(768), 0, s,
+                               (const bf16_t*)a.A, a.lda, (const bf16_t*)a.B, a.ldb, a.M, a.N, a.K, a.K, a.ws, epi);
+        else
             hipLaunchKernelGGL((gemm_bf16_big_kernel<128, 128, 2, 2, PAIRED, false, Epi>), grid, dim3(256), 0, s,
                                (const bf16_t*)a.A, a.lda, (const bf16_t*)a.B, a.ldb, a.M, a.N, a.K, a.K, a.ws, epi);
-        }
         return;
     }
     if (p.dec) {
