@@ -20,6 +20,8 @@
 //   the fp32 path, 64-key chunks merged by a second kernel in chunk order.
 #include <math.h>
 
+#include <type_traits>
+
 #include "kernels.h"
 
 namespace ebrl {
@@ -94,26 +96,47 @@ __global__ __launch_bounds__(64 * NW) void attn_prefill_bf16_kernel(AttnPrefillA
 
     // DMA of key tile `it`: row q of the tile = key k0 + q, its 16-byte chunk
     // c stored at chunk position q * CPR + (c ^ (q & 7)); the waves split the
-    // tile's 64 / RPI instructions for K and the same for V.
+    // tile's 64 / RPI instructions for K and the same for V, so that wave w
+    // fills rows 16 w .. 16 w + 15, i.e. exactly one 16-token cache block.
     static_assert((KT / RPI) % NW == 0, "DMA split");
+    static_assert(KT == 16 * NW && KV_BLOCK == 16, "one cache block per wave and tile");
+    constexpr int NI = KT / RPI;             // instructions per operand
     const size_t blk_elems = (size_t)2 * hkv * KV_BLOCK * HD;
     const bf16_t* kbase = (const bf16_t*)a.kv.base + (size_t)kvh * KV_BLOCK * HD;
     const size_t voff = (size_t)hkv * KV_BLOCK * HD;
     const uint32_t sk_addr = (uint32_t)(uintptr_t)(attn_lds_ptr_t)&sK[0][0];
     const uint32_t sv_addr = (uint32_t)(uintptr_t)(attn_lds_ptr_t)&sV[0][0];
+    const int row_in = lane / CPR, cpos = lane % CPR;
     auto dma = [&](int it, int buf) {
-        constexpr int NI = KT / RPI;             // instructions per operand
-        const int row_in = lane / CPR, cpos = lane % CPR;
+        const int blk_key0 = it * KT + wave * 16;     // first key of this wave's block
+        if (blk_key0 + 16 <= kv_end) {
+            // whole block in range: its address is uniform over the wave
+            const int blk = __builtin_amdgcn_readfirstlane(s_bt[blk_key0 >> 4]);
+            const bf16_t* kb = kbase + (size_t)blk * blk_elems;
 #pragma unroll
-        for (int u = 0; u < NI / NW; ++u) {
-            const int ins = wave * (NI / NW) + u;
-            const int q = ins * RPI + row_in;
-            const int key = min(it * KT + q, kv_end - 1);
-            const int c = cpos ^ (q & 7);
-            const bf16_t* src = kbase + (size_t)s_bt[key >> 4] * blk_elems + (size_t)(key & 15) * HD + c * 8;
-            const uint32_t off = (uint32_t)(buf * TILE + ins * 512) * 2;
-            attn_dma16(src, __builtin_amdgcn_readfirstlane(sk_addr + off));
-            attn_dma16(src + voff, __builtin_amdgcn_readfirstlane(sv_addr + off));
+            for (int u = 0; u < NI / NW; ++u) {
+                const int ins = wave * (NI / NW) + u;
+                const int q = ins * RPI + row_in;
+                const int c = cpos ^ (q & 7);
+                const bf16_t* src = kb + (size_t)((q & 15) * HD + c * 8);
+                const uint32_t off = (uint32_t)(buf * TILE + ins * 512) * 2;
+                attn_dma16(src, __builtin_amdgcn_readfirstlane(sk_addr + off));
+                attn_dma16(src + voff, __builtin_amdgcn_readfirstlane(sv_addr + off));
+            }
+        } else {
+            // the block holding the last keys: rows past them repeat the
+            // last key (finite values; their scores are masked)
+#pragma unroll
+            for (int u = 0; u < NI / NW; ++u) {
+                const int ins = wave * (NI / NW) + u;
+                const int q = ins * RPI + row_in;
+                const int key = min(it * KT + q, kv_end - 1);
+                const int c = cpos ^ (q & 7);
+                const bf16_t* src = kbase + (size_t)s_bt[key >> 4] * blk_elems + (size_t)(key & 15) * HD + c * 8;
+                const uint32_t off = (uint32_t)(buf * TILE + ins * 512) * 2;
+                attn_dma16(src, __builtin_amdgcn_readfirstlane(sk_addr + off));
+                attn_dma16(src + voff, __builtin_amdgcn_readfirstlane(sv_addr + off));
+            }
         }
     };
 
@@ -122,19 +145,21 @@ __global__ __launch_bounds__(64 * NW) void attn_prefill_bf16_kernel(AttnPrefillA
     for (int i = 0; i < HD / 16; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
     float m_i = -INFINITY, l_i = 0.f;
 
-    if (ntiles > 0) dma(0, 0);
-    for (int it = 0; it < ntiles; ++it) {
+    // One key tile from LDS buffer BUF (a compile-time constant, so that
+    // every fragment address is a per-lane base plus an immediate offset).
+    auto tile = [&](int it, auto BUF) {
+        constexpr int buf = decltype(BUF)::value;
         // tile `it` has landed for every wave, and every wave is done with
         // tile it - 1, whose buffer the next DMA refills
         __builtin_amdgcn_s_waitcnt(0);
         __syncthreads();
-        if (it + 1 < ntiles) dma(it + 1, (it + 1) & 1);
-        const bf16_t* tk = sK[it & 1];
-        const bf16_t* tv = sV[it & 1];
+        if (it + 1 < ntiles) dma(it + 1, buf ^ 1);
+        const bf16_t* tk = sK[buf];
+        const bf16_t* tv = sV[buf];
         const int k0 = it * KT;
         // no query of this wave sees a key of this tile: nothing to add
         // (processing it would leave m, l and acc as they are)
-        if (k0 >= wave_keys) continue;
+        if (k0 >= wave_keys) return;
 
         // S^T tiles: lane holds key 16kt + 4g + v for query r
         f32x4 s[4];
@@ -235,6 +260,12 @@ __global__ __launch_bounds__(64 * NW) void attn_prefill_bf16_kernel(AttnPrefillA
                 acc[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, pb, acc[dt], 0, 0, 0);
             }
         }
+    };
+
+    if (ntiles > 0) dma(0, 0);
+    for (int it = 0; it < ntiles; it += 2) {
+        tile(it, std::integral_constant<int, 0>{});
+        if (it + 1 < ntiles) tile(it + 1, std::integral_constant<int, 1>{});
     }
 
     if (qvalid) {
