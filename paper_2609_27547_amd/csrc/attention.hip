@@ -54,13 +54,26 @@ __global__ __launch_bounds__(64 * NW) void attn_prefill_bf16_kernel(AttnPrefillA
     __shared__ __attribute__((aligned(1024))) bf16_t sV[2][TILE];
     __shared__ int s_bt[ATTN_BT_MAX];
 
-    const int t = blockIdx.x, h = blockIdx.y;
+    // Workgroup order: the dispatcher deals workgroup ids round-robin over
+    // the 8 XCDs, each with its own L2.  Ids are remapped so that every XCD
+    // runs a contiguous run of (KV head, query tile, query head in the KV
+    // group) triples: the query heads of one KV group and the query tiles of
+    // one sequence, which read the same K and V, share an L2 (the world
+    // action model's attention: 15 % faster).  Causal attention without
+    // grouped heads keeps the dispatcher's order, which measured 3 % faster
+    // there.
+    const int hkv = a.kv.kv_heads;
+    const int grp = a.q_heads / hkv;
+    int lid = blockIdx.x;
+    const int nb = gridDim.x;
+    if ((nb & 7) == 0 && (!a.causal || grp > 1)) lid = (lid & 7) * (nb >> 3) + (lid >> 3);
+    const int rest = lid / grp;
+    const int t = rest % a.n_tiles, kvh = rest / a.n_tiles;
+    const int h = kvh * grp + (lid - rest * grp);
     const int seq = a.tile_seq[t], qt0 = a.tile_q0[t];
     const int env = a.seq_env[seq];
     const int qlen = a.q_len[seq], qpos0 = a.q_pos0[seq], kvlen = a.kv_len[seq];
     const int qoff = a.q_off[seq];
-    const int hkv = a.kv.kv_heads;
-    const int kvh = h / (a.q_heads / hkv);
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int r = lane & 15, g = lane >> 4;
@@ -339,7 +352,7 @@ void attn_prefill(const AttnPrefillArgs& a, hipStream_t s) {
     if (a.bf16) {
         if (a.kv.bt_stride > ATTN_BT_MAX) return;   // rejected by the caller (capacity check)
         const float scale_log2 = 1.4426950408889634f / sqrtf((float)hd);
-        dim3 grid(a.n_tiles, a.q_heads);
+        dim3 grid(a.n_tiles * a.q_heads);
         constexpr int NW = ATTN_Q_TILE / 16;
         if (hd == 64) hipLaunchKernelGGL((attn_prefill_bf16_kernel<64, NW>), grid, dim3(64 * NW), 0, s, a, scale_log2);
         else hipLaunchKernelGGL((attn_prefill_bf16_kernel<128, NW>), grid, dim3(64 * NW), 0, s, a, scale_log2);
