@@ -143,14 +143,25 @@ int ebrl_prefill(ebrl_policy* p, const ebrl_obs_batch* obs, const int32_t* env_i
 int ebrl_decode_actions(ebrl_policy* p, const int32_t* env_ids, int32_t n, int32_t* out_tokens,
                         float* out_actions, float* out_margin);
 
+/* Seeded noise streams (Philox4x32-10 counter word 3) of the denoising calls. */
+#define EBRL_NOISE_STREAM_ACTIONS 3u
+#define EBRL_NOISE_STREAM_FRAMES 4u
+
 /* Flow-matching action-chunk denoising for n prefilled envs: from
  * x_0 = noise, ten Euler steps x_{k+1} = x_k - v(x_k, tau_k)/10 with
  * tau_k = 1 - k/10, where v is the action expert attending to the env's
  * backbone KV cache layer by layer plus its own chunk tokens.
- * noise: device float32 [n, chunk, adim]; out_actions: device float32
- * [n, chunk, adim] (may alias noise).  EBRL_E_UNSUPPORTED without an
- * expert or for a world action model (frame_tokens > 0: use
- * ebrl_wam_denoise), EBRL_E_STATE for an env with no prefix. */
+ * noise: device float32 [n, chunk, adim], or NULL to draw it on the device:
+ * env e's chunk, flattened, takes element pairs (2j, 2j + 1) from
+ * Philox4x32-10 with key (low, high word of the policy seed) and counter
+ * (j, c_e, e, EBRL_NOISE_STREAM_ACTIONS), Box-Muller on u = (x + 1/2) 2^-32
+ * of the first two output words in double, rounded to float; c_e counts
+ * env e's earlier calls with NULL noise (0 after ebrl_policy_create), so an
+ * env's noise does not depend on the other envs of a call.
+ * out_actions: device float32 [n, chunk, adim] (may alias noise).
+ * EBRL_E_UNSUPPORTED without an expert or for a world action model
+ * (frame_tokens > 0: use ebrl_wam_denoise), EBRL_E_STATE for an env with
+ * no prefix, EBRL_E_INVALID for a NULL out_actions. */
 int ebrl_flow_denoise(ebrl_policy* p, const int32_t* env_ids, int32_t n, const float* noise,
                       float* out_actions);
 
@@ -164,7 +175,10 @@ int ebrl_flow_denoise(ebrl_policy* p, const int32_t* env_ids, int32_t n, const f
  * W_fout [frame_dim, exp_d]; actions as in ebrl_flow_denoise.
  * frame_noise / out_frames: device float32 [n, frame_tokens, frame_dim];
  * action_noise / out_actions: device float32 [n, chunk, adim] (outputs may
- * alias their noise).  EBRL_E_UNSUPPORTED unless frame_tokens > 0. */
+ * alias their noise).  A NULL noise pointer draws that noise on the device
+ * as ebrl_flow_denoise does, frames on EBRL_NOISE_STREAM_FRAMES; the env's
+ * call count advances once per call that draws either.
+ * EBRL_E_UNSUPPORTED unless frame_tokens > 0. */
 int ebrl_wam_denoise(ebrl_policy* p, const int32_t* env_ids, int32_t n, const float* frame_noise,
                      const float* action_noise, float* out_frames, float* out_actions);
 

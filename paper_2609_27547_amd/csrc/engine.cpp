@@ -40,7 +40,8 @@ struct StackDims { int n = 0, d = 0, hq = 0, hkv = 0, hd = 0, mlp = 0; };
 
 struct ProfRec { int cls; hipEvent_t a, b; double flop, bytes; };
 
-struct EnvSlot { int T = 0; std::vector<int> blocks; };
+// T: prefix length; noise_calls: the env's denoise calls that drew seeded noise
+struct EnvSlot { int T = 0; std::vector<int> blocks; uint32_t noise_calls = 0; };
 
 }  // namespace
 
@@ -620,14 +621,18 @@ int denoise(ebrl_policy* p, const int32_t* env_ids, int32_t n, const float* fnoi
     int rc;
     if ((rc = check_ids(p, env_ids, n, true))) return rc;
     if (n == 0) return EBRL_OK;
-    if (!anoise || !aout) return fail(p, EBRL_E_INVALID, "noise / out_actions is NULL");
+    if (!aout) return fail(p, EBRL_E_INVALID, "out_actions is NULL");
     const int F = c.frame_tokens, S = F + c.chunk;
+    // NULL noise: drawn on the device from the policy seed, the env id and
+    // the env's count of such calls (frames on their own stream)
+    const bool seeded = !anoise || (F && !fnoise);
     const int rows = n * S, arows = n * c.chunk, frows = n * F;
     std::vector<int> seq_env(env_ids, env_ids + n), q_off(n), q_len(n, S), q_pos0(n), kv_len(n),
-        row_seq(rows), row_pos(rows), tseq, tq0;
+        row_seq(rows), row_pos(rows), tseq, tq0, calls(n);
     int maxkv = 0;
     for (int i = 0; i < n; ++i) {
         const int T = p->envs[env_ids[i]].T;
+        calls[i] = (int)p->envs[env_ids[i]].noise_calls;
         q_off[i] = i * S;
         q_pos0[i] = T;
         kv_len[i] = T + S;
@@ -638,7 +643,7 @@ int denoise(ebrl_policy* p, const int32_t* env_ids, int32_t n, const float* fnoi
     Meta m;
     const size_t o_env = m.add(seq_env), o_off = m.add(q_off), o_len = m.add(q_len), o_pos0 = m.add(q_pos0),
                  o_kvl = m.add(kv_len), o_rseq = m.add(row_seq), o_rpos = m.add(row_pos), o_tseq = m.add(tseq),
-                 o_tq0 = m.add(tq0);
+                 o_tq0 = m.add(tq0), o_calls = m.add(calls);
     int* md = nullptr;
     if ((rc = upload_meta(p, m, false, &md))) return rc;
     auto body = [&]() -> int {
@@ -646,8 +651,12 @@ int denoise(ebrl_policy* p, const int32_t* env_ids, int32_t n, const float* fnoi
         prof_begin(p, EBRL_K_OTHER);
         small_linear(p->bf16, p->temb, c.n_steps, c.exp_d, p->w_t1, c.exp_d, p->tmid, false, p->stream);
         small_linear(p->bf16, p->tmid, c.n_steps, c.exp_d, p->w_t2, c.exp_d, p->tvec, true, p->stream);
-        copy_f32(anoise, p->flow_x, (size_t)arows * c.adim, p->stream);
-        if (F) copy_f32(fnoise, p->flow_f, (size_t)frows * c.frame_dim, p->stream);
+        if (anoise) copy_f32(anoise, p->flow_x, (size_t)arows * c.adim, p->stream);
+        else normal_noise(p->flow_x, n, c.chunk * c.adim, md + o_env, md + o_calls, p->seed, EBRL_NOISE_STREAM_ACTIONS,
+                          p->stream);
+        if (F && fnoise) copy_f32(fnoise, p->flow_f, (size_t)frows * c.frame_dim, p->stream);
+        else if (F) normal_noise(p->flow_f, n, F * c.frame_dim, md + o_env, md + o_calls, p->seed,
+                                 EBRL_NOISE_STREAM_FRAMES, p->stream);
         prof_end(p, 0, 0);
         for (int k = 0; k < c.n_steps; ++k) {
             const float* tv = p->tvec + (size_t)k * c.exp_d;
@@ -687,6 +696,8 @@ int denoise(ebrl_policy* p, const int32_t* env_ids, int32_t n, const float* fnoi
     const int inside = (1 << EBRL_K_GEMM) | (1 << EBRL_K_GEMM_SKINNY) | (1 << EBRL_K_ATTN_PREFILL) |
                        (1 << EBRL_K_OTHER);
     if ((rc = run_graph(p, key, inside, body))) return rc;
+    if (seeded)
+        for (int i = 0; i < n; ++i) ++p->envs[env_ids[i]].noise_calls;
     p->last_flow_ids.assign(env_ids, env_ids + n);
     return check_launch(p);
 }
@@ -1243,7 +1254,7 @@ int ebrl_wam_denoise(ebrl_policy* p, const int32_t* env_ids, int32_t n, const fl
     if (rc) return rc;
     if (!p->cfg.exp_layers || !p->cfg.frame_tokens)
         return fail(p, EBRL_E_UNSUPPORTED, "policy has no future-frame tokens");
-    if (n > 0 && (!frame_noise || !out_frames)) return fail(p, EBRL_E_INVALID, "frame_noise / out_frames is NULL");
+    if (n > 0 && !out_frames) return fail(p, EBRL_E_INVALID, "out_frames is NULL");
     return denoise(p, env_ids, n, frame_noise, action_noise, out_frames, out_actions);
 }
 

@@ -568,6 +568,61 @@ void copy_f32(const float* src, float* dst, size_t n, hipStream_t s) {
 }
 
 
+// ---------------------------------------------------------- seeded noise --
+// Philox4x32-10 (Salmon, Moraes, Dror, Shaw, SC'11), ten rounds of
+//   (c0, c1, c2, c3) <- (mulhi(B, c2) ^ c1 ^ k0, mullo(B, c2),
+//                        mulhi(A, c0) ^ c3 ^ k1, mullo(A, c0)),
+// A = 0xD2511F53, B = 0xCD9E8D57, key bumped by (0x9E3779B9, 0xBB67AE85)
+// before every round but the first; then Box-Muller (1958) on the first two
+// words, u = (x + 1/2) 2^-32, in double, rounded to float.  Row i's pair j
+// takes counter (j, calls[i], env[i], stream) under key (lo, hi of seed).
+__device__ __forceinline__ void philox4x32_10(uint32_t c[4], uint32_t k0, uint32_t k1) {
+#pragma unroll
+    for (int r = 0; r < 10; ++r) {
+        if (r) {
+            k0 += 0x9E3779B9u;
+            k1 += 0xBB67AE85u;
+        }
+        const uint32_t hb = __umulhi(0xCD9E8D57u, c[2]), lb = 0xCD9E8D57u * c[2];
+        const uint32_t ha = __umulhi(0xD2511F53u, c[0]), la = 0xD2511F53u * c[0];
+        const uint32_t n0 = hb ^ c[1] ^ k0, n2 = ha ^ c[3] ^ k1;
+        c[0] = n0;
+        c[1] = lb;
+        c[2] = n2;
+        c[3] = la;
+    }
+}
+
+__global__ __launch_bounds__(256) void normal_noise_kernel(float* __restrict__ out, int per_row,
+                                                           const int* __restrict__ env,
+                                                           const int* __restrict__ calls, uint32_t k0,
+                                                           uint32_t k1, uint32_t stream) {
+    const int i = blockIdx.y;
+    const int pairs = (per_row + 1) / 2;
+    const uint32_t e = (uint32_t)env[i], call = (uint32_t)calls[i];
+    for (int j = blockIdx.x * blockDim.x + threadIdx.x; j < pairs; j += gridDim.x * blockDim.x) {
+        uint32_t c[4] = {(uint32_t)j, call, e, stream};
+        philox4x32_10(c, k0, k1);
+        const double u1 = ((double)c[0] + 0.5) * (1.0 / 4294967296.0);
+        const double u2 = ((double)c[1] + 0.5) * (1.0 / 4294967296.0);
+        const double rad = sqrt(-2.0 * log(u1));
+        const double ang = 6.283185307179586 * u2;
+        float* o = out + (size_t)i * per_row + 2 * j;
+        o[0] = (float)(rad * cos(ang));
+        if (2 * j + 1 < per_row) o[1] = (float)(rad * sin(ang));
+    }
+}
+
+void normal_noise(float* out, int rows, int per_row, const int* env, const int* calls, uint64_t seed,
+                  uint32_t stream, hipStream_t s) {
+    if (rows <= 0 || per_row <= 0) return;
+    const int pairs = (per_row + 1) / 2;
+    dim3 grid((unsigned)std::min((pairs + 255) / 256, 64), (unsigned)rows);
+    hipLaunchKernelGGL(normal_noise_kernel, grid, dim3(256), 0, s, out, per_row, env, calls,
+                       (uint32_t)(seed & 0xFFFFFFFFu), (uint32_t)(seed >> 32), stream);
+}
+
+
 // ------------------------------------------------------- streaming read --
 // Workgroup b reads 16-byte words [b * per, (b + 1) * per) with eight
 // non-temporal loads in flight per lane.  A lane writes *out only if the XOR

@@ -430,22 +430,29 @@ class Policy:
                     "decode_actions")
         return tokens, actions, margins
 
-    def flow_denoise(self, env_ids, noise, out=None):
-        torch = self.torch
+    def _chunk_out(self, n, rows, cols):
+        return self.torch.empty((n, rows, cols), dtype=self.torch.float32, device="cuda")
+
+    def flow_denoise(self, env_ids, noise=None, out=None):
+        """noise None: the library draws it (seeded, per-env call count)."""
         ids, pids = _ids(env_ids)
         if out is None:
-            out = torch.empty_like(noise)
+            out = self._chunk_out(len(ids), self.cfg.chunk, self.cfg.adim) if noise is None else \
+                self.torch.empty_like(noise)
         self._check(lib().ebrl_flow_denoise(self.h, pids, len(ids), _ptr(noise), _ptr(out)), "flow_denoise")
         return out
 
-    def wam_denoise(self, env_ids, frame_noise, action_noise, out_frames=None, out_actions=None):
-        """Joint denoising of future-frame latents and the action chunk."""
-        torch = self.torch
+    def wam_denoise(self, env_ids, frame_noise=None, action_noise=None, out_frames=None, out_actions=None):
+        """Joint denoising of future-frame latents and the action chunk;
+        a noise of None is drawn by the library."""
         ids, pids = _ids(env_ids)
+        c = self.cfg
         if out_frames is None:
-            out_frames = torch.empty_like(frame_noise)
+            out_frames = self._chunk_out(len(ids), c.frame_tokens, c.frame_dim) if frame_noise is None else \
+                self.torch.empty_like(frame_noise)
         if out_actions is None:
-            out_actions = torch.empty_like(action_noise)
+            out_actions = self._chunk_out(len(ids), c.chunk, c.adim) if action_noise is None else \
+                self.torch.empty_like(action_noise)
         self._check(lib().ebrl_wam_denoise(self.h, pids, len(ids), _ptr(frame_noise), _ptr(action_noise),
                                            _ptr(out_frames), _ptr(out_actions)), "wam_denoise")
         return out_frames, out_actions

@@ -34,6 +34,7 @@ _MASK = np.uint64(0xFFFFFFFF)
 STREAM_PIXELS = 1
 STREAM_LANG = 2
 STREAM_NOISE = 3
+STREAM_FRAMES = 4
 
 
 def philox4x32_10(c0, c1, c2, c3, seed: int):
@@ -87,16 +88,19 @@ def lang_ids(obs_seed: int, env_ids, count: int, vocab: int) -> np.ndarray:
     return out
 
 
-def flow_noise(seed: int, env_ids, chunk: int, adim: int) -> np.ndarray:
-    """float32 standard-normal noise ``[n, chunk, adim]`` (Box-Muller on Philox)."""
+def flow_noise(seed: int, env_ids, chunk: int, adim: int, call: int = 0, stream: int = STREAM_NOISE) -> np.ndarray:
+    """float32 standard-normal noise ``[n, chunk, adim]`` (Box-Muller on Philox):
+    env e's element pair j takes counter (j, call, e, stream) under key seed,
+    the convention the library follows when it draws the noise itself
+    (``call`` = the env's earlier such calls; frames use stream 4)."""
     count = chunk * adim
     out = np.empty((len(env_ids), count), dtype=np.float32)
     pairs = (count + 1) // 2
-    j = np.arange(pairs, dtype=np.uint64)
-    lo = (j & _MASK).astype(np.uint32)
-    hi = (j >> np.uint64(32)).astype(np.uint32)
+    assert pairs < 2 ** 32
+    lo = np.arange(pairs, dtype=np.uint32)
+    hi = np.full(pairs, call, dtype=np.uint32)
     for i, e in enumerate(env_ids):
-        x0, x1, _, _ = philox4x32_10(lo, hi, np.uint32(int(e)), np.uint32(STREAM_NOISE), seed)
+        x0, x1, _, _ = philox4x32_10(lo, hi, np.uint32(int(e)), np.uint32(stream), seed)
         u1 = (x0.astype(np.float64) + 0.5) * 2.0 ** -32
         u2 = (x1.astype(np.float64) + 0.5) * 2.0 ** -32
         r = np.sqrt(-2.0 * np.log(u1))

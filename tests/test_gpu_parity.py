@@ -334,6 +334,49 @@ def test_tiny_flow_bf16_parity_and_zero_output_closed_form():
     pol.close()
 
 
+def test_tiny_flow_seeded_noise_closed_form_and_parity():
+    """NULL noise: the library draws it on the device (Philox4x32-10 keyed by
+    the policy seed, counter (pair, the env's count of such calls, env id,
+    stream 3), Box-Muller).  The full model on that noise matches the oracle
+    fed the harness's draw of it; with W_aout = 0 the chunk comes out as the
+    noise itself, which pins the device generator against the harness's
+    numpy one to one float ulp (both round a double Box-Muller value whose
+    log/cos may differ in the last double bit), for every env whatever else
+    the call holds, with each env's count advancing per call."""
+    o = TINY_FLOW
+    seed = 7
+    ids = [0, 2, 3]
+    img, lang = _obs(o, ids, 1004)
+    pol = E.Policy(_ebrl_config(o, 4), seed=seed)
+    pol.prefill(ids, images=_dev(img), lang_ids=_dev(lang))
+    out = pol.flow_denoise(ids)                         # every env's call 0
+    torch.cuda.synchronize()
+    out = out.cpu().numpy()
+    nz = synth_inputs.flow_noise(seed, ids, o.chunk, o.adim, call=0)
+    ref = M.Policy(o, seed=seed)
+    for i in range(len(ids)):
+        st = ref.prefill(img[i], lang[i])
+        assert P.row_rel_err(out[i], ref.flow_denoise(st, nz[i])) < P.TOL_BF16
+    tid, shape = M.tensor_shapes(o)["W_aout"]
+    pol.write_weight(tid, np.zeros(shape, np.uint16))
+    calls = {0: 1, 2: 1, 3: 1}
+    for batch in ([2], [3, 0], [0, 2, 3], [2]):
+        got = pol.flow_denoise(batch)
+        torch.cuda.synchronize()
+        got = got.cpu().numpy()
+        for i, e in enumerate(batch):
+            want = synth_inputs.flow_noise(seed, [e], o.chunk, o.adim, call=calls[e])[0]
+            np.testing.assert_array_max_ulp(got[i], want, maxulp=1)
+            calls[e] += 1
+    # caller-supplied noise neither uses nor advances the count
+    given = synth_inputs.flow_noise(11, [2], o.chunk, o.adim)
+    assert np.array_equal(pol.flow_denoise([2], _dev(given)).cpu().numpy(), given)
+    got = pol.flow_denoise([2]).cpu().numpy()
+    np.testing.assert_array_max_ulp(got[0], synth_inputs.flow_noise(seed, [2], o.chunk, o.adim,
+                                                                    call=calls[2])[0], maxulp=1)
+    pol.close()
+
+
 # ----------------------------------------------------- tiny world action model --
 
 TINY_WAM = M.Config("tinywam", bf16=True, n_cams=1, img=32, patch=16, layers=2, d=128, q_heads=4,
@@ -372,6 +415,29 @@ def test_tiny_wam_bf16_parity_and_closed_forms():
     f0, a0 = pol.wam_denoise(ids, _dev(nf), _dev(na))
     torch.cuda.synchronize()
     assert np.array_equal(f0.cpu().numpy(), nf) and np.array_equal(a0.cpu().numpy(), na)
+    pol.close()
+
+
+def test_tiny_wam_seeded_noise_closed_form():
+    # both noises drawn by the library, frames on stream 4, one count per
+    # env advanced once per call; zero output projections return them as is
+    o = TINY_WAM
+    seed = 9
+    ids = [1, 3]
+    img, lang = _obs(o, ids, 1005)
+    pol = E.Policy(_ebrl_config(o, 4), seed=seed)
+    pol.prefill(ids, images=_dev(img), lang_ids=_dev(lang))
+    for name in ("W_aout", "W_fout"):
+        tid, shape = M.tensor_shapes(o)[name]
+        pol.write_weight(tid, np.zeros(shape, np.uint16))
+    for call in range(2):
+        f, a = pol.wam_denoise(ids)
+        torch.cuda.synchronize()
+        wf = synth_inputs.flow_noise(seed, ids, o.frame_tokens, o.frame_dim, call=call,
+                                     stream=synth_inputs.STREAM_FRAMES)
+        wa = synth_inputs.flow_noise(seed, ids, o.chunk, o.adim, call=call)
+        np.testing.assert_array_max_ulp(f.cpu().numpy(), wf, maxulp=1)
+        np.testing.assert_array_max_ulp(a.cpu().numpy(), wa, maxulp=1)
     pol.close()
 
 
