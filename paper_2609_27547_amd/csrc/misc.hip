@@ -465,41 +465,53 @@ EBRL_DEV size_t flow_row(int r, int per_in, int per_out, int off) {
     return (size_t)(r / per_in) * per_out + off + r % per_in;
 }
 
-// A workgroup projects FLOW_IN_ROWS tokens: their inputs sit in LDS and each
-// thread keeps one output's weight row in registers while it walks the rows,
-// so the weights are read once per workgroup instead of once per token.  Each
-// output is summed over the input channels in channel order.
-constexpr int FLOW_IN_ROWS = 64;
+// A workgroup projects FLOW_IN_ROWS tokens onto 256 of the d outputs (grid:
+// row blocks x output slices, so that even a few thousand tokens fill the
+// chip): the tokens' inputs sit in LDS, each thread keeps its output's
+// weight row in registers and runs four tokens at a time (independent FMA
+// chains).  Each output is summed over the input channels in channel order,
+// then the time embedding is added.
+constexpr int FLOW_IN_ROWS = 16;
 template <typename T, int AMAX>
-__global__ __launch_bounds__(256) void flow_in_kernel(const float* x, int rows, int adim, const T* W_ain,
-                                                      const float* tvec, int d, float* H, int ldh,
-                                                      int per_in, int per_out, int off)
+__global__ __launch_bounds__(256) void flow_in_kernel(const float* __restrict__ x, int rows, int adim,
+                                                      const T* __restrict__ W_ain, const float* __restrict__ tvec,
+                                                      int d, float* __restrict__ H, int ldh, int per_in,
+                                                      int per_out, int off)
 {
+    static_assert(FLOW_IN_ROWS % 4 == 0, "four tokens per pass");
     __shared__ float sx[FLOW_IN_ROWS * AMAX];
     const int r0 = blockIdx.x * FLOW_IN_ROWS;
     const int nr = min(FLOW_IN_ROWS, rows - r0);
-    for (int i = threadIdx.x; i < nr * adim; i += blockDim.x) sx[i] = x[(size_t)r0 * adim + i];
+    for (int i = threadIdx.x; i < FLOW_IN_ROWS * AMAX; i += blockDim.x) {
+        const int q = i / AMAX, j = i - q * AMAX;
+        sx[i] = (q < nr && j < adim) ? x[(size_t)(r0 + q) * adim + j] : 0.f;
+    }
     __syncthreads();
-    for (int o = threadIdx.x; o < d; o += blockDim.x) {
-        float w[AMAX];
+    const int o = blockIdx.y * blockDim.x + threadIdx.x;
+    if (o >= d) return;
+    float w[AMAX];
 #pragma unroll
-        for (int j = 0; j < AMAX; ++j) w[j] = j < adim ? ld_elem<T>(W_ain + (size_t)o * adim + j) : 0.f;
-        const float t = tvec[o];
-        for (int q = 0; q < nr; ++q) {
-            const float* xr = sx + q * adim;
-            float acc = 0.f;
+    for (int j = 0; j < AMAX; ++j) w[j] = j < adim ? ld_elem<T>(W_ain + (size_t)o * adim + j) : 0.f;
+    const float t = tvec[o];
+    for (int q0 = 0; q0 < nr; q0 += 4) {
+        float acc[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-            for (int j = 0; j < AMAX; ++j)
-                if (j < adim) acc = fmaf(w[j], xr[j], acc);
-            H[flow_row(r0 + q, per_in, per_out, off) * ldh + o] = acc + t;
+        for (int j = 0; j < AMAX; ++j) {
+            if (j < adim) {
+#pragma unroll
+                for (int u = 0; u < 4; ++u) acc[u] = fmaf(w[j], sx[(q0 + u) * AMAX + j], acc[u]);
+            }
         }
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+            if (q0 + u < nr) H[flow_row(r0 + q0 + u, per_in, per_out, off) * ldh + o] = acc[u] + t;
     }
 }
 
 void flow_in(bool bf16, const float* x, int rows, int adim, const void* W_ain, const float* tvec,
              int d, float* H, int ldh, int per_in, int per_out, int off, hipStream_t s) {
     if (rows <= 0) return;
-    const dim3 grid((rows + FLOW_IN_ROWS - 1) / FLOW_IN_ROWS);
+    const dim3 grid((rows + FLOW_IN_ROWS - 1) / FLOW_IN_ROWS, (d + 255) / 256);
     auto go = [&](auto amax) {
         constexpr int AM = decltype(amax)::value;
         if (bf16)
