@@ -555,10 +555,108 @@ __global__ __launch_bounds__(256) void flow_out_kernel(const float* H, int ldh, 
     }
 }
 
+// The same projection with RW rows per wave (four waves per workgroup):
+// each lane holds columns 256 i + 4 lane .. + 3 of its rows in registers, a
+// weight row is loaded once for all of them, and every dot product and
+// sum of squares is summed per lane in column order, then over the lanes
+// (wave_sum).  For d a multiple of 256 up to 2048.
+template <typename T, int D4, int RW>
+__global__ __launch_bounds__(256) void flow_out_rows_kernel(const float* __restrict__ H, int ldh, int d,
+                                                            const T* __restrict__ W_aout, int adim, float eps,
+                                                            float n_steps, float* __restrict__ x,
+                                                            float* __restrict__ v_out, int rows, int per_in,
+                                                            int per_out, int off)
+{
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const int r0 = (blockIdx.x * 4 + wave) * RW;
+    float4 hv[RW][D4];
+#pragma unroll
+    for (int k = 0; k < RW; ++k) {
+        float ss = 0.f;
+        if (r0 + k < rows) {
+            const float* h = H + flow_row(r0 + k, per_in, per_out, off) * ldh + 4 * lane;
+#pragma unroll
+            for (int i = 0; i < D4; ++i) {
+                hv[k][i] = *reinterpret_cast<const float4*>(h + 256 * i);
+                ss = fmaf(hv[k][i].x, hv[k][i].x, ss);
+                ss = fmaf(hv[k][i].y, hv[k][i].y, ss);
+                ss = fmaf(hv[k][i].z, hv[k][i].z, ss);
+                ss = fmaf(hv[k][i].w, hv[k][i].w, ss);
+            }
+        } else {
+#pragma unroll
+            for (int i = 0; i < D4; ++i) hv[k][i] = make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+        ss = wave_sum(ss);
+        const float rs = 1.0f / sqrtf(ss / (float)d + eps);
+#pragma unroll
+        for (int i = 0; i < D4; ++i) {
+            hv[k][i].x *= rs; hv[k][i].y *= rs; hv[k][i].z *= rs; hv[k][i].w *= rs;
+        }
+    }
+    float mine[RW];
+#pragma unroll
+    for (int k = 0; k < RW; ++k) mine[k] = 0.f;
+    for (int c = 0; c < adim; ++c) {
+        const T* wr = W_aout + (size_t)c * d + 4 * lane;
+        float acc[RW];
+#pragma unroll
+        for (int k = 0; k < RW; ++k) acc[k] = 0.f;
+#pragma unroll
+        for (int i = 0; i < D4; ++i) {
+            float w[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) w[e] = ld_elem<T>(wr + 256 * i + e);
+#pragma unroll
+            for (int k = 0; k < RW; ++k) {
+                acc[k] = fmaf(w[0], hv[k][i].x, acc[k]);
+                acc[k] = fmaf(w[1], hv[k][i].y, acc[k]);
+                acc[k] = fmaf(w[2], hv[k][i].z, acc[k]);
+                acc[k] = fmaf(w[3], hv[k][i].w, acc[k]);
+            }
+        }
+#pragma unroll
+        for (int k = 0; k < RW; ++k) {
+            const float v = wave_sum(acc[k]);
+            if (lane == c) mine[k] = v;
+        }
+    }
+#pragma unroll
+    for (int k = 0; k < RW; ++k) {
+        const int r = r0 + k;
+        if (r < rows && lane < adim) {
+            x[(size_t)r * adim + lane] -= mine[k] / n_steps;
+            if (v_out) v_out[(size_t)r * adim + lane] = mine[k];
+        }
+    }
+}
+
 void flow_out(bool bf16, const float* H, int ldh, int rows, int d, const void* W_aout, int adim,
               float eps, float n_steps, float* x, float* v_out, int per_in, int per_out, int off,
               hipStream_t s) {
     if (rows <= 0) return;
+    auto go = [&](auto d4, auto rw) {
+        constexpr int D4 = decltype(d4)::value, RW = decltype(rw)::value;
+        const dim3 grid((rows + 4 * RW - 1) / (4 * RW));
+        if (bf16)
+            hipLaunchKernelGGL((flow_out_rows_kernel<bf16_t, D4, RW>), grid, dim3(256), 0, s, H, ldh, d,
+                               (const bf16_t*)W_aout, adim, eps, n_steps, x, v_out, rows, per_in, per_out, off);
+        else
+            hipLaunchKernelGGL((flow_out_rows_kernel<float, D4, RW>), grid, dim3(256), 0, s, H, ldh, d,
+                               (const float*)W_aout, adim, eps, n_steps, x, v_out, rows, per_in, per_out, off);
+    };
+    using std::integral_constant;
+    if (d % 256 == 0 && adim <= 64) {
+        switch (d / 256) {
+        case 1: go(integral_constant<int, 1>{}, integral_constant<int, 4>{}); return;
+        case 2: go(integral_constant<int, 2>{}, integral_constant<int, 4>{}); return;
+        case 3: go(integral_constant<int, 3>{}, integral_constant<int, 4>{}); return;
+        case 4: go(integral_constant<int, 4>{}, integral_constant<int, 4>{}); return;
+        case 6: go(integral_constant<int, 6>{}, integral_constant<int, 2>{}); return;
+        case 8: go(integral_constant<int, 8>{}, integral_constant<int, 2>{}); return;
+        default: break;
+        }
+    }
     const size_t shm = (size_t)(d + adim) * sizeof(float);
     if (bf16)
         hipLaunchKernelGGL(flow_out_kernel<bf16_t>, dim3(rows), dim3(256), shm, s, H, ldh, d,

@@ -3,6 +3,8 @@
 Inputs are the seeded synthetic observations of synth_inputs; expected
 values come only from the CPU oracle (oracle/).  Criteria in tests/parity.py.
 """
+import dataclasses
+
 import numpy as np
 import pytest
 
@@ -309,8 +311,9 @@ TINY_FLOW = M.Config("tinyflow", bf16=True, n_cams=1, img=32, patch=16, layers=2
                      exp_layers=2, exp_d=128, exp_heads=2, exp_mlp=256, chunk=50, adim=7, n_steps=10)
 
 
-def test_tiny_flow_bf16_parity_and_zero_output_closed_form():
-    o = TINY_FLOW
+@pytest.mark.parametrize("exp_d", [128, 256])   # 256: the multi-row output projection
+def test_tiny_flow_bf16_parity_and_zero_output_closed_form(exp_d):
+    o = dataclasses.replace(TINY_FLOW, exp_d=exp_d)
     ids = [0, 2, 3]
     img, lang = _obs(o, ids, 1004)
     noise = synth_inputs.flow_noise(4, ids, o.chunk, o.adim)
@@ -385,10 +388,11 @@ TINY_WAM = M.Config("tinywam", bf16=True, n_cams=1, img=32, patch=16, layers=2, 
                     frame_tokens=70, frame_dim=16)
 
 
-def test_tiny_wam_bf16_parity_and_closed_forms():
+@pytest.mark.parametrize("exp_d", [128, 256])
+def test_tiny_wam_bf16_parity_and_closed_forms(exp_d):
     # 70 frame tokens + 50 action tokens: two query tiles per env, the
-    # second ragged
-    o = TINY_WAM
+    # second ragged; exp_d 256 takes the multi-row output projection
+    o = dataclasses.replace(TINY_WAM, exp_d=exp_d)
     ids = [0, 2, 3]
     img, lang = _obs(o, ids, 1005)
     nf = synth_inputs.flow_noise(5, ids, o.frame_tokens, o.frame_dim)
