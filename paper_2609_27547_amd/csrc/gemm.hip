@@ -84,40 +84,53 @@ template <typename T> struct EpiQKV {
     T* Q; int ldq; T* kv; const int* bt; int bt_stride; int hq, hkv, hd;
     const int* seq_env; const int* row_seq; const int* row_pos;
     const float* cos_tab; const float* sin_tab; int use_rope;
-    EBRL_DEV void pair(int m, int n, const float* x1, const float* x2) const {
+    // Per-row part of the destination: the row's position and the element
+    // offset of its token row in head 0's K block (paged cache).
+    EBRL_DEV int4 row_info(int m) const {
+        const int pos = row_pos[m];
+        const int env = seq_env[row_seq[m]];
+        const int blk = bt[(size_t)env * bt_stride + (pos >> 4)];
+        const size_t off = (size_t)blk * 2 * hkv * KV_BLOCK * hd + (size_t)(pos & 15) * hd;
+        return make_int4(pos, (int)(uint32_t)off, (int)(uint32_t)(off >> 32), 0);
+    }
+    EBRL_DEV void pair_at(int4 ri, int m, int n, const float* x1, const float* x2) const {
         const int qn = hq * hd, kn = hkv * hd;
         const int region = n < qn ? 0 : (n < qn + kn ? 1 : 2);
         const int local = n - (region == 0 ? 0 : (region == 1 ? qn : qn + kn));
         const int h = local / hd, pc = local - h * hd;
         const int e = (pc >> 5) * 16 + (pc & 15);
         const int half = hd >> 1;
-        const int pos = row_pos[m];
+        const int pos = ri.x;
         float a[4], b[4];
 #pragma unroll
         for (int t = 0; t < 4; ++t) { a[t] = x1[t]; b[t] = x2[t]; }
         if (region < 2 && use_rope) {
-            const float* ct = cos_tab + (size_t)pos * half + e;
-            const float* st = sin_tab + (size_t)pos * half + e;
+            const float4 c = *reinterpret_cast<const float4*>(cos_tab + (size_t)pos * half + e);
+            const float4 sn = *reinterpret_cast<const float4*>(sin_tab + (size_t)pos * half + e);
+            const float cc[4] = {c.x, c.y, c.z, c.w}, ss[4] = {sn.x, sn.y, sn.z, sn.w};
 #pragma unroll
             for (int t = 0; t < 4; ++t) {
-                const float c = ct[t], sn = st[t];
-                a[t] = x1[t] * c - x2[t] * sn;
-                b[t] = x2[t] * c + x1[t] * sn;
+                a[t] = x1[t] * cc[t] - x2[t] * ss[t];
+                b[t] = x2[t] * cc[t] + x1[t] * ss[t];
             }
         }
         T* dst;
         if (region == 0) {
             dst = Q + (size_t)m * ldq + h * hd;
         } else {
-            const int env = seq_env[row_seq[m]];
-            const int blk = bt[(size_t)env * bt_stride + (pos >> 4)];
-            dst = kv + (size_t)blk * 2 * hkv * KV_BLOCK * hd + ((size_t)(region == 2 ? hkv : 0) + h) * KV_BLOCK * hd +
-                  (size_t)(pos & 15) * hd;
+            const size_t off = (size_t)(uint32_t)ri.y | ((size_t)(uint32_t)ri.z << 32);
+            dst = kv + off + ((size_t)(region == 2 ? hkv : 0) + h) * KV_BLOCK * hd;
         }
         st4<T>(dst + e, a[0], a[1], a[2], a[3]);
         st4<T>(dst + e + half, b[0], b[1], b[2], b[3]);
     }
+    EBRL_DEV void pair(int m, int n, const float* x1, const float* x2) const {
+        pair_at(row_info(m), m, n, x1, x2);
+    }
 };
+// Epilogues whose per-row work the large-M kernel hoists out of the column loop.
+template <class E> struct epi_row_info : std::false_type {};
+template <typename T> struct epi_row_info<EpiQKV<T>> : std::true_type {};
 template <typename T> EpiQKV<T> make_epi_qkv(const RopeKVArgs& r) {
     return EpiQKV<T>{(T*)r.Q, r.ldq, (T*)r.kv.base, r.kv.block_table, r.kv.bt_stride, r.q_heads,
                      r.kv.kv_heads, r.kv.head_dim, r.seq_env, r.row_seq, r.row_pos, r.cos_tab, r.sin_tab,
@@ -436,6 +449,11 @@ __global__ __launch_bounds__(64 * WM * WN, WM * WN == 4 ? 2 : 1) void gemm_bf16_
     constexpr int SROW = 68;
     constexpr int PER_A = (BM * 64 * 2) / (16 * SROW * 4), PER_B = (BN * 64 * 2) / (16 * SROW * 4);
     static_assert(2 * (PER_A + PER_B) >= NW, "staging space");
+    static_assert(WTM == 64, "one row per lane in the per-row epilogue data");
+    // per-row epilogue data of the wave's 64 rows, one row per lane
+    __shared__ int4 s_row[epi_row_info<Epi>::value ? NW : 1][64];
+    if constexpr (epi_row_info<Epi>::value)
+        s_row[wave][lane] = epi.row_info(min(m0 + wm * WTM + lane, M - 1));
     bf16_t* const region = wave < PER_A ? sA0 : (wave < 2 * PER_A ? sA1 : (wave < 2 * PER_A + PER_B ? sB0 : sB1));
     const int slot = wave < PER_A ? wave : (wave < 2 * PER_A ? wave - PER_A
                                             : (wave < 2 * PER_A + PER_B ? wave - 2 * PER_A : wave - 2 * PER_A - PER_B));
@@ -459,7 +477,8 @@ __global__ __launch_bounds__(64 * WM * WN, WM * WN == 4 ? 2 : 1) void gemm_bf16_
                 if (m < M && n < N) {
                     float gv[4] = {gv4[0], gv4[1], gv4[2], gv4[3]};
                     float uv[4] = {uv4[0], uv4[1], uv4[2], uv4[3]};
-                    epi.pair(m, n, gv, uv);
+                    if constexpr (epi_row_info<Epi>::value) epi.pair_at(s_row[wave][i * 16 + row], m, n, gv, uv);
+                    else epi.pair(m, n, gv, uv);
                 }
             }
         } else {
