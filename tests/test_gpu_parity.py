@@ -471,6 +471,36 @@ def test_tiny_vit_bf16_parity():
     pol.close()
 
 
+def test_bf16_prefill_batch_invariance_bitwise():
+    """bf16 prefill: an env's prefix state, KV and tokens do not depend on
+    the batch -- 16 envs (320 rows: the large-M GEMM kernel) against 3 of
+    them (60 rows: the small-M kernel) in another order, bitwise, since both
+    kernels sum K in the same 64-wide steps; and within the oracle
+    tolerance."""
+    o = TINY_VIT
+    ids = list(range(16))
+    img, lang = _obs(o, ids, 1007)
+    pol = E.Policy(_ebrl_config(o, 16), seed=0)
+    pol.prefill(ids, images=_dev(img), lang_ids=_dev(lang))
+    tok_all, _, mar_all = pol.decode_actions(ids)
+    torch.cuda.synchronize()
+    sub = [11, 2, 7]
+    pol2 = E.Policy(_ebrl_config(o, 16), seed=0)
+    pol2.prefill(sub, images=_dev(img[sub]), lang_ids=_dev(lang[sub]))
+    tok, _, mar = pol2.decode_actions(sub)
+    torch.cuda.synchronize()
+    ref = M.Policy(o, seed=0)
+    for j, e in enumerate(sub):
+        h = pol2.read_state(E.STATE_H_LAST_PRE, e)
+        assert np.array_equal(h, pol.read_state(E.STATE_H_LAST_PRE, e))
+        assert np.array_equal(pol2.read_state(E.STATE_K, e, 1), pol.read_state(E.STATE_K, e, 1))
+        assert torch.equal(tok[j], tok_all[e]) and torch.equal(mar[j], mar_all[e])
+        st = ref.prefill(img[e], lang[e])
+        assert P.row_rel_err(h, st.h_last_pre) < P.TOL_BF16
+    pol.close()
+    pol2.close()
+
+
 def test_stream_read_reference_kernel():
     # the HBM read reference: argument checks, and a run that reads every
     # byte without writing its output (the fold of 1-filled words is not the
