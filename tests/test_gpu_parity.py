@@ -501,6 +501,38 @@ def test_bf16_prefill_batch_invariance_bitwise():
     pol2.close()
 
 
+TINY_LANG = M.Config("tinylang", bf16=True, n_cams=0, img=32, patch=16, layers=2, d=128, q_heads=4,
+                     kv_heads=2, head_dim=64, mlp=256, vocab=100, n_lang=130)
+
+
+@pytest.mark.parametrize("hd", [64, 128])
+def test_bf16_attention_at_block_and_tile_boundaries(hd):
+    """Language-only bf16 prefixes on either side of the 16-token cache
+    blocks and the 64-key attention tiles (lengths 1, 15, 16, 17, 63, 64, 65,
+    129), head dim 64 (4 query heads over 2 KV heads) and 128 (2 over 1):
+    prefix state, the second layer's K rows and the decoded tokens (whose
+    keys cross the same boundaries) against the oracle."""
+    o = dataclasses.replace(TINY_LANG, head_dim=hd, q_heads=4 if hd == 64 else 2,
+                            kv_heads=2 if hd == 64 else 1)
+    lens = [1, 15, 16, 17, 63, 64, 65, 129]
+    ids = list(range(len(lens)))
+    _, lang = _obs(o, ids, 1008)
+    pol = E.Policy(_ebrl_config(o, len(ids)), seed=0)
+    pol.prefill(ids, images=None, lang_ids=_dev(lang), lang_len=lens)
+    tok, _, _ = pol.decode_actions(ids)
+    torch.cuda.synchronize()
+    tok = tok.cpu().numpy()
+    ref = M.Policy(o, seed=0)
+    for e, T in zip(ids, lens):
+        st = ref.prefill(None, lang[e][:T])
+        assert int(pol.read_state(E.STATE_PREFIX_LEN, e)[0]) == T
+        assert P.row_rel_err(pol.read_state(E.STATE_H_LAST_PRE, e), st.h_last_pre) < P.TOL_BF16
+        k = P.bf16_to_f64(pol.read_state(E.STATE_K, e, 1))
+        assert P.row_rel_err(k.reshape(T, -1), st.k[1].reshape(T, -1)) < P.TOL_BF16
+        P.check_tokens(tok[e], ref.decode(st, forced=tok[e, :-1]))
+    pol.close()
+
+
 def test_stream_read_reference_kernel():
     # the HBM read reference: argument checks, and a run that reads every
     # byte without writing its output (the fold of 1-filled words is not the
