@@ -39,6 +39,27 @@ EBRL_DEV void attn_dma16(const void* g, uint32_t lds_addr) {
                  :: "v"(g), "s"(lds_addr) : "memory", "m0");
 }
 
+// Lanes l and l ^ 16, then l and l ^ 32, combined with VALU lane swaps
+// (v_permlane16_swap / v_permlane32_swap hand each lane both values of its
+// pair), instead of LDS-routed swizzles that queue behind the K/V traffic.
+// Both lanes of a pair get the same result (the operations commute).
+EBRL_DEV float attn_max_xor16_32(float v) {
+    const unsigned u = __builtin_bit_cast(unsigned, v);
+    const auto a = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+    v = fmaxf(__builtin_bit_cast(float, (unsigned)a[0]), __builtin_bit_cast(float, (unsigned)a[1]));
+    const unsigned w = __builtin_bit_cast(unsigned, v);
+    const auto b = __builtin_amdgcn_permlane32_swap(w, w, false, false);
+    return fmaxf(__builtin_bit_cast(float, (unsigned)b[0]), __builtin_bit_cast(float, (unsigned)b[1]));
+}
+EBRL_DEV float attn_sum_xor16_32(float v) {
+    const unsigned u = __builtin_bit_cast(unsigned, v);
+    const auto a = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+    v = __builtin_bit_cast(float, (unsigned)a[0]) + __builtin_bit_cast(float, (unsigned)a[1]);
+    const unsigned w = __builtin_bit_cast(unsigned, v);
+    const auto b = __builtin_amdgcn_permlane32_swap(w, w, false, false);
+    return __builtin_bit_cast(float, (unsigned)b[0]) + __builtin_bit_cast(float, (unsigned)b[1]);
+}
+
 // One workgroup per (query tile of ATTN_Q_TILE rows, head): NW waves of 16
 // queries share every K/V tile staged in LDS, which each wave then skips if
 // none of its queries can see it.
@@ -210,8 +231,7 @@ __global__ __launch_bounds__(64 * NW) void attn_prefill_bf16_kernel(AttnPrefillA
 #pragma unroll
                 for (int v = 0; v < 4; ++v) tmax = fmaxf(tmax, s[kt][v]);
         }
-        tmax = fmaxf(tmax, swz_xor16_f(tmax));
-        tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
+        tmax = attn_max_xor16_32(tmax);
         // The running maximum is kept as an integer (ceil, in log2 units):
         // rescaling by alpha is then a power of two, which commutes with the
         // bf16 rounding of P, so P is rounded as 2^(x - ceil(row max)) no
@@ -228,8 +248,7 @@ __global__ __launch_bounds__(64 * NW) void attn_prefill_bf16_kernel(AttnPrefillA
                 s[kt][v] = p;
                 psum += p;
             }
-        psum += swz_xor16_f(psum);
-        psum += __shfl_xor(psum, 32, 64);
+        psum = attn_sum_xor16_32(psum);
         l_i = l_i * alpha + psum;
         m_i = m_new;
         // alpha is a power of two that is 1 once the integer running maximum
