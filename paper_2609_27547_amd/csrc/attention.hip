@@ -129,7 +129,9 @@ __global__ __launch_bounds__(64 * NW) void attn_prefill_bf16_kernel(AttnPrefillA
     __syncthreads();
 
     // DMA of key tile `it`: row q of the tile = key k0 + q, its 16-byte chunk
-    // c stored at chunk position q * CPR + (c ^ (q & 7)); the waves split the
+    // c stored at chunk position q * CPR + (c ^ (q % CPR)) -- the XOR spans
+    // every chunk of a row, so that 8 (hd 64) or 16 (hd 128) consecutive rows
+    // put a given chunk on all 64 LDS banks; the waves split the
     // tile's 64 / RPI instructions for K and the same for V, so that wave w
     // fills rows 16 w .. 16 w + 15, i.e. exactly one 16-token cache block.
     static_assert((KT / RPI) % NW == 0, "DMA split");
@@ -151,7 +153,7 @@ __global__ __launch_bounds__(64 * NW) void attn_prefill_bf16_kernel(AttnPrefillA
             for (int u = 0; u < NI / NW; ++u) {
                 const int ins = wave * (NI / NW) + u;
                 const int q = ins * RPI + row_in;
-                const int c = cpos ^ (q & 7);
+                const int c = cpos ^ (q & (CPR - 1));
                 const bf16_t* src = kb + (size_t)((q & 15) * HD + c * 8);
                 const uint32_t off = (uint32_t)(buf * TILE + ins * 512) * 2;
                 attn_dma16(src, __builtin_amdgcn_readfirstlane(sk_addr + off));
@@ -165,7 +167,7 @@ __global__ __launch_bounds__(64 * NW) void attn_prefill_bf16_kernel(AttnPrefillA
                 const int ins = wave * (NI / NW) + u;
                 const int q = ins * RPI + row_in;
                 const int key = min(it * KT + q, kv_end - 1);
-                const int c = cpos ^ (q & 7);
+                const int c = cpos ^ (q & (CPR - 1));
                 const bf16_t* src = kbase + (size_t)s_bt[key >> 4] * blk_elems + (size_t)(key & 15) * HD + c * 8;
                 const uint32_t off = (uint32_t)(buf * TILE + ins * 512) * 2;
                 attn_dma16(src, __builtin_amdgcn_readfirstlane(sk_addr + off));
@@ -204,7 +206,7 @@ __global__ __launch_bounds__(64 * NW) void attn_prefill_bf16_kernel(AttnPrefillA
 #pragma unroll
             for (int ks = 0; ks < HD / 32; ++ks) {
                 const bf16x8 ka =
-                    *reinterpret_cast<const bf16x8*>(tk + (row * CPR + ((ks * 4 + g) ^ (row & 7))) * 8);
+                    *reinterpret_cast<const bf16x8*>(tk + (row * CPR + ((ks * 4 + g) ^ (row & (CPR - 1)))) * 8);
                 s[kt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka, qb[ks], s[kt], 0, 0, 0);
             }
         }
@@ -278,12 +280,12 @@ __global__ __launch_bounds__(64 * NW) void attn_prefill_bf16_kernel(AttnPrefillA
                 attn_v4s lo, hi;
                 {
                     const int key = 32 * ks2 + 4 * g + (a16 >> 2);
-                    const int off = (key * CPR + ((d >> 3) ^ (key & 7))) * 8 + (d & 7);
+                    const int off = (key * CPR + ((d >> 3) ^ (key & (CPR - 1)))) * 8 + (d & 7);
                     lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) attn_v4s*)(attn_lds_ptr_t)(tv + off));
                 }
                 {
                     const int key = 32 * ks2 + 16 + 4 * g + (a16 >> 2);
-                    const int off = (key * CPR + ((d >> 3) ^ (key & 7))) * 8 + (d & 7);
+                    const int off = (key * CPR + ((d >> 3) ^ (key & (CPR - 1)))) * 8 + (d & 7);
                     hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) attn_v4s*)(attn_lds_ptr_t)(tv + off));
                 }
                 const uint2 lo2 = __builtin_bit_cast(uint2, lo), hi2 = __builtin_bit_cast(uint2, hi);
