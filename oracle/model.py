@@ -381,10 +381,12 @@ class Policy:
                  cache_limit_params: int = 600_000_000, emulate_bf16: bool = False):
         self.cfg = cfg
         self.seed = seed
-        # Optional: round to bf16 exactly where a bf16 policy stores bf16
-        # (normalised GEMM inputs, rotated Q and K, V, softmax numerators
-        # before the P.V product, attention and SwiGLU outputs, patch pixels);
-        # all arithmetic between those points stays float64.  Off by default.
+        # Optional diagnostic: round to bf16 where a bf16 policy stores
+        # activations in bf16 (normalised GEMM inputs, rotated Q and K, V,
+        # softmax numerators before the P.V product, attention and SwiGLU
+        # outputs, patch pixels); all arithmetic between those points stays
+        # float64.  Off by default; parity is always judged against the exact
+        # mode, never against this one.
         self.emulate_bf16 = bool(emulate_bf16 and cfg.bf16)
         self.shapes = tensor_shapes(cfg)
         self.overrides = dict(overrides or {})
@@ -415,27 +417,20 @@ class Policy:
         return {s: self.W(f"{kind}.{l}.{s}") for s in SLOT}
 
     # blocks ----------------------------------------------------------------
-    def _prenorm(self, x, folded):
-        """Operand of the projection after a pre-norm, and the row factor its
-        output is multiplied by.  Without bf16 emulation this is RMSNorm then
-        the product, exactly.  Emulating the bf16 policy's decode steps
-        (``folded``), the operand is the residual row rounded to bf16 and the
-        RMSNorm factor of that rounded row scales the product's rows;
-        otherwise the normalised row is rounded."""
-        if self.emulate_bf16 and folded:
-            h = self._r(x)
-            return h, 1.0 / np.sqrt(np.mean(h * h, axis=-1, keepdims=True) + self.cfg.eps)
-        return self._r(rmsnorm(x, self.cfg.eps)), 1.0
+    def _prenorm(self, x):
+        """Operand of the projection after a pre-norm: the normalised row
+        (rounded to bf16 when emulating bf16 storage)."""
+        return self._r(rmsnorm(x, self.cfg.eps))
 
     def block(self, x, Wl, n_heads, n_kv, hd, pos, past_k=None, past_v=None, past_pos=None,
-              causal=True, use_rope=True, folded=False):
+              causal=True, use_rope=True):
         """Pre-norm transformer block.  Returns (x_out, k_new, v_new)."""
         t = x.shape[0]
         R = self._r
-        h, f = self._prenorm(x, folded)
-        q = (linear(h, Wl["q"]) * f).reshape(t, n_heads, hd)
-        k = (linear(h, Wl["k"]) * f).reshape(t, n_kv, hd)
-        v = (linear(h, Wl["v"]) * f).reshape(t, n_kv, hd)
+        h = self._prenorm(x)
+        q = linear(h, Wl["q"]).reshape(t, n_heads, hd)
+        k = linear(h, Wl["k"]).reshape(t, n_kv, hd)
+        v = linear(h, Wl["v"]).reshape(t, n_kv, hd)
         if use_rope:
             q = rope(q, pos, self.cfg.rope_base)
             k = rope(k, pos, self.cfg.rope_base)
@@ -452,8 +447,8 @@ class Policy:
             o = multihead_attention(q, K, V, pos, kpos, causal)
         o = R(o.reshape(t, n_heads * hd))
         x = x + linear(o, Wl["o"])
-        h, f = self._prenorm(x, folded)
-        x = x + linear(R(silu(linear(h, Wl["gate"]) * f) * (linear(h, Wl["up"]) * f)), Wl["down"])
+        h = self._prenorm(x)
+        x = x + linear(R(silu(linear(h, Wl["gate"])) * linear(h, Wl["up"])), Wl["down"])
         return x, k, v
 
     def _r(self, a):
@@ -461,12 +456,9 @@ class Policy:
 
     @staticmethod
     def _attention_bf16(q, k, v, q_pos, k_pos, causal):
-        """Softmax attention whose numerators enter the P.V product rounded to
-        bf16 while the denominator sums the unrounded ones (the bf16 policy's
-        storage points).  The numerators are taken relative to the power of
-        two at or above the row maximum: with x = s log2(e), e_j = 2^(x_j -
-        ceil(max x)).  The scale cancels in the ratio, so without rounding
-        this is exactly `attention`."""
+        """Softmax attention whose numerators exp(s - max s) enter the P.V
+        product rounded to bf16 while the denominator sums the unrounded
+        ones (bf16 storage of P).  Without rounding this is `attention`."""
         hq, hkv, hd = q.shape[1], k.shape[1], q.shape[-1]
         out = np.empty_like(q)
         for h in range(hq):
@@ -474,8 +466,7 @@ class Policy:
             s = (q[:, h, :] @ k[:, g, :].T) / np.sqrt(hd)
             if causal:
                 s = np.where(k_pos[None, :] <= q_pos[:, None], s, -np.inf)
-            x = s * np.log2(np.e)
-            e = np.exp2(x - np.ceil(np.max(x, axis=-1, keepdims=True)))
+            e = np.exp(s - np.max(s, axis=-1, keepdims=True))
             out[:, h, :] = (f64_to_bf16_value(e) @ v[:, g, :]) / np.sum(e, axis=-1, keepdims=True)
         return out
 
@@ -571,7 +562,7 @@ class Policy:
             pos = np.array([st.T + step - 1])
             for l in range(cfg.layers):
                 x, k, v = self.block(x, self.layer("dec", l), cfg.q_heads, cfg.kv_heads,
-                                     cfg.head_dim, pos, ks[l], vs[l], kpos, folded=True)
+                                     cfg.head_dim, pos, ks[l], vs[l], kpos)
                 ks[l] = np.concatenate([ks[l], k], axis=0)
                 vs[l] = np.concatenate([vs[l], v], axis=0)
             kpos = np.concatenate([kpos, pos])
