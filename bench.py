@@ -5,9 +5,10 @@ A step is one pass of the whole hot path over one batch of synthetic
 observations: prefill (patch embedding, language embedding, every decoder
 layer writing the paged KV cache) followed by the autoregressive action
 decode (t0 from the prefix, six decode steps over the paged cache, 256-bin
-argmax).  The default workload is the small bf16 VLA on 64 environments
-(two 224x224 cameras, 32 language tokens, 12-layer d=1024 decoder); every
-step yields one 7-dim action per environment.
+argmax).  The default workload is the 7B-class VLA on 32 environments (one
+224x224 camera through a 24-layer ViT, 32 language tokens, 32-layer d=4096
+decoder), the largest configuration that is timed as prefill + decode on one
+GPU; every step yields one 7-dim action per environment.
 
 Output: one JSON line with the throughput (actions/s), the roofline entry of
 the dominant kernel (the prefill GEMMs, timed live with HIP events on the
@@ -201,7 +202,7 @@ def colocated(E, torch, w, args):
     def gen_run(s_ptr):
         ext_g = torch.cuda.ExternalStream(s_ptr)
         if args.workload == "ragged-7b":
-            w.call_i = args.warmup
+            w.call_i = 0
         g0, g1 = _events(torch, 2)
         g0.record(ext_g)
         n_act = 0
@@ -402,10 +403,21 @@ class Workload:
             self.T = synth_inputs.ragged_prefix_lengths(5, n, 200, 320)
             lang = synth_inputs.lang_ids(seed, ids, 320, c.vocab)
             self.pol.prefill(ids, images=None, lang_ids=dev(lang), lang_len=self.T)
+            # the seeded call sequence (n ~ U[1, 128] distinct ids per call);
+            # timed regions always start at its first call
             self.calls = synth_inputs.ragged_calls(5, max(steps, 1), n, 128)
             self.call_i = 0
             self.tok = torch.empty((128, c.n_action_tokens), dtype=torch.int32, device="cuda")
             self.act = torch.empty((128, c.n_action_tokens), dtype=torch.float32, device="cuda")
+            # set-up, untimed: one call per batch-size class, which captures
+            # the decode graph of every class once (as a server would at start)
+            t = time.perf_counter()
+            sizes = sorted({k if k <= 4 else min(128, (k + 7) // 8 * 8) for k in range(1, 129)})
+            for k in sizes:
+                self.pol.decode_actions(ids[:k], tokens=self.tok[:k], actions=self.act[:k], margins=None,
+                                        with_margin=False)
+            torch.cuda.synchronize()
+            log(f"ragged-7b: {len(sizes)} batch-size classes captured in {time.perf_counter() - t:.1f} s")
             return
         self.img = dev(synth_inputs.pixels(seed, ids, c.n_cams, c.img, c.img))
         self.lang = dev(synth_inputs.lang_ids(seed, ids, c.n_lang, c.vocab))
@@ -449,7 +461,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="small-bf16", choices=sorted(WORKLOADS))
+    ap.add_argument("--workload", default="7b-bf16", choices=sorted(WORKLOADS))
     ap.add_argument("--cpu-sample", type=int, default=None,
                     help="envs in the oracle sample (0 = skip; default: about 10-40 s of oracle work)")
     ap.add_argument("--partitions", action="store_true",
@@ -472,7 +484,7 @@ def main():
 
     torch.cuda.set_device(0)
     stream = torch.cuda.current_stream()
-    w = Workload(args.workload, E, torch, args.steps + args.warmup + 2)
+    w = Workload(args.workload, E, torch, args.steps)
     pol, c = w.pol, w.c
     for _ in range(args.warmup):
         w.step()
@@ -488,6 +500,8 @@ def main():
     dominant = max(classes, key=lambda k: pre[k]["ms"])
 
     # ---- timed region: K steps; the dominant kernel class timed live with HIP events
+    if args.workload == "ragged-7b":
+        w.call_i = 0
     pol.profile_read(dominant, reset=True)
     pol.profile_enable([dominant])
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -539,6 +553,15 @@ def main():
                              "tflops": round(r["flop"] / (r["ms"] * 1e9), 1) if r["ms"] else None,
                              "gbs": round(r["bytes"] / (r["ms"] * 1e6), 1) if r["ms"] else None}
 
+    # roofline fraction of every kernel class (breakdown pass, per-launch events)
+    fractions = {}
+    for name, k in kernels.items():
+        if name in ("gemm", "attn_prefill") and k["tflops"] is not None:
+            fractions[name] = {"bound": "mfma", "achieved_tflops": k["tflops"],
+                               "frac": round(k["tflops"] / (PEAK_BF16_TFLOPS if pol.bf16 else PEAK_FP32_TFLOPS), 4)}
+        elif name in ("gemm_skinny", "attn_decode") and k["gbs"] is not None:
+            fractions[name] = {"bound": "hbm", "achieved_gbs": k["gbs"], "frac": round(k["gbs"] / PEAK_HBM_GBS, 4)}
+
     # ---- optional: the same steps on CU-masked partitions (the stand-in for SM quotas)
     partitions = None
     read_bw = {}
@@ -555,7 +578,7 @@ def main():
             try:
                 pol.bind_stream(s_ptr)
                 if args.workload == "ragged-7b":
-                    w.call_i = args.warmup
+                    w.call_i = 0
                 torch.cuda.synchronize()
                 t0 = time.perf_counter()
                 n_act = sum(w.step() for _ in range(args.steps))
@@ -609,7 +632,7 @@ def main():
     preset, n, _ = WORKLOADS[args.workload]
     if args.workload == "ragged-7b":
         desc = (f"ragged-7b: preset 3 (7B-class), pool of 128 language-only prefixes (T ~ U[200, 320]), "
-                f"{args.steps} decode calls of n ~ U[1, 128] envs")
+                f"the first {args.steps} decode calls of the seeded sequence, n ~ U[1, 128] envs each")
     elif c.frame_tokens:
         desc = (f"{args.workload}: preset {preset}, {n} envs, prefix {c.max_seq} tokens, {c.layers}-layer "
                 f"d={c.d} backbone + {c.n_steps} Euler steps of the {c.exp_layers}-layer diffusion transformer over "
@@ -637,6 +660,7 @@ def main():
         "gpu_ms_per_step": round(gpu_ms / args.steps, 3),
         "phases_ms": {k: round(v, 3) for k, v in phase.items()},
         "kernels": kernels,
+        "class_roofline_fractions": fractions,
         "roofline": roofline,
         "cpu_baseline": base,
     }

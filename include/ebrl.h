@@ -93,7 +93,9 @@ typedef struct ebrl_obs_batch {
     int32_t lang_stride;      /* row stride of lang_ids in elements (>= every lang_len) */
 } ebrl_obs_batch;
 
-/* Fill *out with preset 1..5 (1 tiny fp32 VLA, 2 small bf16 VLA, 3 7B-class
+/* Paper: Section 2.1 names the model families; Section 6.1 the models the
+ * workloads stand in for (no sizes are given, the presets are readings).
+ * Fill *out with preset 1..5 (1 tiny fp32 VLA, 2 small bf16 VLA, 3 7B-class
  * bf16 VLA with ViT, 4 flow-matching expert on a GQA backbone, 5 world
  * action model: preset 4's backbone and expert denoising two future frames
  * of 7 x 7 latent tokens (32 channels) with the action chunk); capacity
@@ -101,7 +103,9 @@ typedef struct ebrl_obs_batch {
  * EBRL_E_INVALID for any other preset. */
 int ebrl_config_preset(int32_t preset, ebrl_config* out);
 
-/* Create a policy on the current HIP device: validates *config, generates
+/* Paper: Section 2.1 (the policy the generation stage runs); the KV budget
+ * is the memory share m of a GPU-CPU resource pool (Section 4.3.1).
+ * Create a policy on the current HIP device: validates *config, generates
  * the seeded random-init weights (Philox4x32-10 + Box-Muller, N(0, std^2),
  * bf16 by nearest-even rounding of the fp32 value), uploads them and
  * allocates the paged KV pool (16-token blocks) and scratch.  *out receives
@@ -111,7 +115,9 @@ int ebrl_policy_create(const ebrl_config* config, uint64_t seed, ebrl_policy** o
 /* Synchronises the bound stream and frees everything the policy owns. */
 void ebrl_policy_destroy(ebrl_policy* p);
 
-/* Create a stream restricted to the compute units whose bits are set in
+/* Paper: Section 4.3.1 (per-stage GPU quota s) and Section 5 (quotas fixed
+ * when a worker is launched).
+ * Create a stream restricted to the compute units whose bits are set in
  * cu_mask (n_words 32-bit words, bit k of word w = CU 32*w + k in the
  * runtime's enumeration) on `device`: the stand-in for the paper's per-stage
  * SM quota.  *out_stream receives a hipStream_t. */
@@ -119,18 +125,24 @@ int ebrl_stream_create_cu_masked(int32_t device, const uint32_t* cu_mask, uint32
                                  void** out_stream);
 int ebrl_stream_destroy(void* stream);
 
-/* All later calls on p enqueue on `stream` (a hipStream_t on p's device;
+/* Paper: Section 4.3.1 (the generation stage runs inside its quota).
+ * All later calls on p enqueue on `stream` (a hipStream_t on p's device;
  * NULL = the null stream). */
 int ebrl_policy_bind_stream(ebrl_policy* p, void* stream);
 
-/* Encode n environments' observations into their KV caches (all decoder
+/* Paper: Section 2.1 (the backbone fuses observations into the KV cache the
+ * action head consumes) and Section 4.2.2 (ragged groups of environments).
+ * Encode n environments' observations into their KV caches (all decoder
  * layers) and remember each env's final-normed last prefix row for the
  * action head.  env_ids: host int32 [n].  Re-prefilling an env replaces its
  * cache.  Errors: EBRL_E_INVALID for bad ids/lengths/shapes or T_i >
  * max_seq, EBRL_E_OOM when the KV budget cannot hold the prefixes. */
 int ebrl_prefill(ebrl_policy* p, const ebrl_obs_batch* obs, const int32_t* env_ids, int32_t n);
 
-/* Autoregressive action decode for n prefilled envs: token t0 = argmax of
+/* Paper: Section 2.1 (the action head produces the action from the cache),
+ * Section 2.2 (generation produces each env's next action) and Section
+ * 4.2.2 (ragged groups).
+ * Autoregressive action decode for n prefilled envs: token t0 = argmax of
  * the 256-bin logits of the last prefix row, then six decode steps, each
  * feeding the previous token's action embedding at the next position.
  * Ties in the argmax go to the lowest bin.  Bin b maps to -1 + (2b+1)/256.
@@ -147,7 +159,10 @@ int ebrl_decode_actions(ebrl_policy* p, const int32_t* env_ids, int32_t n, int32
 #define EBRL_NOISE_STREAM_ACTIONS 3u
 #define EBRL_NOISE_STREAM_FRAMES 4u
 
-/* Flow-matching action-chunk denoising for n prefilled envs: from
+/* Paper: Section 2.1 (an action head that iteratively denoises the action
+ * chunk from the backbone's cache) and Section 3.1 (the lightweight
+ * denoising steps of generation).
+ * Flow-matching action-chunk denoising for n prefilled envs: from
  * x_0 = noise, ten Euler steps x_{k+1} = x_k - v(x_k, tau_k)/10 with
  * tau_k = 1 - k/10, where v is the action expert attending to the env's
  * backbone KV cache layer by layer plus its own chunk tokens.
@@ -165,7 +180,9 @@ int ebrl_decode_actions(ebrl_policy* p, const int32_t* env_ids, int32_t n, int32
 int ebrl_flow_denoise(ebrl_policy* p, const int32_t* env_ids, int32_t n, const float* noise,
                       float* out_actions);
 
-/* World-action-model denoising (Section 2.1: a diffusion transformer that
+/* Paper: Section 2.1 (world action models) and Section 6.1 (the DreamZero
+ * workload).
+ * World-action-model denoising (Section 2.1: a diffusion transformer that
  * jointly denoises latent future frames and the action chunk, each modality
  * with its own decoder): the same Euler schedule as ebrl_flow_denoise over
  * frame_tokens + chunk tokens per env -- frame latents at positions T_e ..
@@ -198,7 +215,10 @@ enum {
     EBRL_STATE_V = 3,           /* KV dtype [T_e, kv_heads, head_dim]: layer's values */
     EBRL_STATE_FLOW_V0 = 4,     /* float32 [chunk, adim]: velocity at tau = 1 of the env's
                                    latest flow call */
-    EBRL_STATE_PREFIX_LEN = 5   /* int32 [1]: T_e, or 0 if the env has no prefix */
+    EBRL_STATE_PREFIX_LEN = 5,  /* int32 [1]: T_e, or 0 if the env has no prefix */
+    EBRL_STATE_GRAPHS = 6       /* int32 [1]: HIP graphs the policy holds (decode graphs are kept per
+                                   batch-size class, denoise graphs per batch size; env_id is
+                                   ignored but must be in range) */
 };
 
 /* Copy one piece of env `env_id`'s state to host memory `out` (capacity

@@ -99,13 +99,22 @@ struct ebrl_policy {
     void* Hb = nullptr;
     void* patches = nullptr;
     float* Vx = nullptr;       // ViT residual stream
-    float* h_pre = nullptr;    // [max_envs, d]
+    float* h_pre = nullptr;    // [max_envs + 1, d] (the last row: the padding env)
     float* h_norm = nullptr;
     float* ws = nullptr;       // split-K workspace
     size_t ws_floats = 0;
     unsigned* counters = nullptr;  // split-K tile counters (zero between calls)
-    float* lg = nullptr;           // action logits scratch [max_envs][n_bins]
+    float* lg = nullptr;           // action logits scratch [dec_cap][n_bins]
     unsigned* lg_counters = nullptr;
+    // Decode calls run on a batch-size class (dec_class): rows past the
+    // call's n are padding rows of env `pad_env` (an internal slot past the
+    // caller's ids with a one-token zero prefix).  Outputs go to these
+    // policy-owned buffers and are copied to the caller's after the graph.
+    int dec_cap = 0;
+    int pad_env = 0;
+    int* dec_tok = nullptr;        // [dec_cap][n_action_tokens]
+    float* dec_act = nullptr;
+    float* dec_mar = nullptr;
     float* part = nullptr;     // decode attention partials
     size_t part_floats = 0;
     float* flow_x = nullptr;
@@ -130,9 +139,11 @@ struct ebrl_policy {
     int cur_cls = -1;
     hipEvent_t cur_a = nullptr;
 
-    // HIP graphs of whole decode / denoise calls, keyed by the call's shape
-    // and output pointers (the per-call metadata lives at fixed offsets of
-    // meta_dev and is refreshed by an async copy before each launch)
+    // HIP graphs of whole decode / denoise calls, keyed by the call's batch
+    // size class (decode) or batch size (denoise) only: the per-call metadata
+    // lives at fixed offsets of meta_dev and is refreshed by an async copy
+    // before each launch, and inputs and outputs pass through policy-owned
+    // buffers outside the graph, so new caller pointers never re-capture
     hipStream_t cap_stream = nullptr;
     std::map<std::vector<uint64_t>, hipGraphExec_t> graphs;
 
@@ -629,14 +640,12 @@ int denoise(ebrl_policy* p, const int32_t* env_ids, int32_t n, const float* fnoi
     const int rows = n * S, arows = n * c.chunk, frows = n * F;
     std::vector<int> seq_env(env_ids, env_ids + n), q_off(n), q_len(n, S), q_pos0(n), kv_len(n),
         row_seq(rows), row_pos(rows), tseq, tq0, calls(n);
-    int maxkv = 0;
     for (int i = 0; i < n; ++i) {
         const int T = p->envs[env_ids[i]].T;
         calls[i] = (int)p->envs[env_ids[i]].noise_calls;
         q_off[i] = i * S;
         q_pos0[i] = T;
         kv_len[i] = T + S;
-        maxkv = std::max(maxkv, kv_len[i]);
         for (int j = 0; j < S; ++j) { row_seq[i * S + j] = i; row_pos[i * S + j] = T + j; }
         for (int q0 = 0; q0 < S; q0 += ATTN_Q_TILE) { tseq.push_back(i); tq0.push_back(q0); }
     }
@@ -646,17 +655,23 @@ int denoise(ebrl_policy* p, const int32_t* env_ids, int32_t n, const float* fnoi
                  o_tq0 = m.add(tq0), o_calls = m.add(calls);
     int* md = nullptr;
     if ((rc = upload_meta(p, m, false, &md))) return rc;
+    // caller noise enters and the result leaves through the policy's own
+    // buffers outside the graph, so the graph never holds a caller pointer
+    prof_begin(p, EBRL_K_OTHER);
+    if (anoise) copy_f32(anoise, p->flow_x, (size_t)arows * c.adim, p->stream);
+    if (F && fnoise) copy_f32(fnoise, p->flow_f, (size_t)frows * c.frame_dim, p->stream);
+    prof_end(p, 0, 0);
     auto body = [&]() -> int {
         // time-MLP outputs for the fixed tau schedule
         prof_begin(p, EBRL_K_OTHER);
         small_linear(p->bf16, p->temb, c.n_steps, c.exp_d, p->w_t1, c.exp_d, p->tmid, false, p->stream);
         small_linear(p->bf16, p->tmid, c.n_steps, c.exp_d, p->w_t2, c.exp_d, p->tvec, true, p->stream);
-        if (anoise) copy_f32(anoise, p->flow_x, (size_t)arows * c.adim, p->stream);
-        else normal_noise(p->flow_x, n, c.chunk * c.adim, md + o_env, md + o_calls, p->seed, EBRL_NOISE_STREAM_ACTIONS,
-                          p->stream);
-        if (F && fnoise) copy_f32(fnoise, p->flow_f, (size_t)frows * c.frame_dim, p->stream);
-        else if (F) normal_noise(p->flow_f, n, F * c.frame_dim, md + o_env, md + o_calls, p->seed,
-                                 EBRL_NOISE_STREAM_FRAMES, p->stream);
+        if (!anoise)
+            normal_noise(p->flow_x, n, c.chunk * c.adim, md + o_env, md + o_calls, p->seed, EBRL_NOISE_STREAM_ACTIONS,
+                         p->stream);
+        if (F && !fnoise)
+            normal_noise(p->flow_f, n, F * c.frame_dim, md + o_env, md + o_calls, p->seed, EBRL_NOISE_STREAM_FRAMES,
+                         p->stream);
         prof_end(p, 0, 0);
         for (int k = 0; k < c.n_steps; ++k) {
             const float* tv = p->tvec + (size_t)k * c.exp_d;
@@ -673,7 +688,7 @@ int denoise(ebrl_policy* p, const int32_t* env_ids, int32_t n, const float* fnoi
                 b.pre.seq_env = md + o_env; b.pre.q_off = md + o_off; b.pre.q_len = md + o_len;
                 b.pre.q_pos0 = md + o_pos0; b.pre.kv_len = md + o_kvl; b.pre.tile_seq = md + o_tseq;
                 b.pre.tile_q0 = md + o_tq0; b.pre.n_tiles = (int)tseq.size(); b.pre.causal = false;
-                b.pre.max_kv_len = maxkv;
+                b.pre.max_kv_len = c.max_seq + S;   // the graph may serve longer prefixes later
                 b.attn_flop = 0;
                 for (int i = 0; i < n; ++i) b.attn_flop += 4.0 * c.head_dim * p->exp.hq * (double)S * kv_len[i];
                 int rc2 = run_block(p, b);
@@ -686,16 +701,19 @@ int denoise(ebrl_policy* p, const int32_t* env_ids, int32_t n, const float* fnoi
                      k == 0 ? p->flow_v0 : nullptr, c.chunk, S, F, p->stream);
             prof_end(p, 0, 0);
         }
-        copy_f32(p->flow_x, aout, (size_t)arows * c.adim, p->stream);
-        if (F) copy_f32(p->flow_f, fout, (size_t)frows * c.frame_dim, p->stream);
         return check_launch(p);
     };
-    const std::vector<uint64_t> key = {2, (uint64_t)n, (uint64_t)maxkv, (uint64_t)(uintptr_t)anoise,
-                                       (uint64_t)(uintptr_t)aout, (uint64_t)(uintptr_t)fnoise,
-                                       (uint64_t)(uintptr_t)fout};
+    // graph per (batch size, which noises are drawn on the device); the key
+    // holds no caller pointer and no prefix length (the attention reads each
+    // sequence's length from the metadata)
+    const std::vector<uint64_t> key = {2, (uint64_t)n, (uint64_t)(anoise ? 1 : 0), (uint64_t)(fnoise ? 1 : 0)};
     const int inside = (1 << EBRL_K_GEMM) | (1 << EBRL_K_GEMM_SKINNY) | (1 << EBRL_K_ATTN_PREFILL) |
                        (1 << EBRL_K_OTHER);
     if ((rc = run_graph(p, key, inside, body))) return rc;
+    prof_begin(p, EBRL_K_OTHER);
+    copy_f32(p->flow_x, aout, (size_t)arows * c.adim, p->stream);
+    if (F) copy_f32(p->flow_f, fout, (size_t)frows * c.frame_dim, p->stream);
+    prof_end(p, 0, 0);
     if (seeded)
         for (int i = 0; i < n; ++i) ++p->envs[env_ids[i]].noise_calls;
     p->last_flow_ids.assign(env_ids, env_ids + n);
@@ -854,18 +872,34 @@ int ebrl_policy_create(const ebrl_config* config, uint64_t seed, ebrl_policy** o
     const size_t block_bytes_all = p->block_elems * p->esz * c.layers;
     int64_t budget = c.kv_budget_bytes;
     if (budget <= 0) budget = (int64_t)block_bytes_all * p->bt_stride * c.max_envs;
-    p->num_blocks = (int)(budget / (int64_t)block_bytes_all);
-    if (p->num_blocks < p->bt_stride) {
-        fail(p, EBRL_E_INVALID, "kv_budget_bytes holds %d blocks, one env needs %d", p->num_blocks, p->bt_stride);
+    const int budget_blocks = (int)(budget / (int64_t)block_bytes_all);
+    if (budget_blocks < p->bt_stride) {
+        fail(p, EBRL_E_INVALID, "kv_budget_bytes holds %d blocks, one env needs %d", budget_blocks, p->bt_stride);
         return bail(EBRL_E_INVALID);
     }
+    // the padding env of decode size classes: a one-token prefix of zeros
+    // plus its action-token slots, in blocks of its own outside the budget
+    p->pad_env = c.max_envs;
+    const int pad_blocks = (1 + p->tail + KV_BLOCK - 1) / KV_BLOCK;
+    p->num_blocks = budget_blocks + pad_blocks;
     if ((rc = dev_alloc(p, &p->kv_pool, (size_t)p->num_blocks * block_bytes_all))) return bail(rc);
-    p->free_blocks.resize(p->num_blocks);
-    for (int b = 0; b < p->num_blocks; ++b) p->free_blocks[b] = p->num_blocks - 1 - b;
-    p->envs.assign(c.max_envs, EnvSlot());
-    p->bt_host.assign((size_t)c.max_envs * p->bt_stride, 0);
+    p->free_blocks.resize(budget_blocks);
+    for (int b = 0; b < budget_blocks; ++b) p->free_blocks[b] = budget_blocks - 1 - b;
+    p->envs.assign(c.max_envs + 1, EnvSlot());
+    p->bt_host.assign((size_t)(c.max_envs + 1) * p->bt_stride, 0);
+    {
+        EnvSlot& pad = p->envs[p->pad_env];
+        pad.T = 1;
+        for (int b = 0; b < pad_blocks; ++b) {
+            pad.blocks.push_back(budget_blocks + b);
+            p->bt_host[(size_t)p->pad_env * p->bt_stride + b] = budget_blocks + b;
+        }
+        for (int l = 0; l < c.layers; ++l)
+            HIPCHK(p, hipMemset((char*)dec_kv(p, l).base + (size_t)budget_blocks * p->block_elems * p->esz, 0,
+                                (size_t)pad_blocks * p->block_elems * p->esz));
+    }
     if ((rc = dev_alloc_t(p, &p->bt_dev, p->bt_host.size()))) return bail(rc);
-    HIPCHK(p, hipMemset(p->bt_dev, 0, p->bt_host.size() * sizeof(int)));
+    HIPCHK(p, hipMemcpy(p->bt_dev, p->bt_host.data(), p->bt_host.size() * sizeof(int), hipMemcpyHostToDevice));
 
     // ---- rotary tables (angles in double on the host, rounded to float)
     {
@@ -904,7 +938,8 @@ int ebrl_policy_create(const ebrl_config* config, uint64_t seed, ebrl_policy** o
     const size_t pre_rows = (size_t)c.max_envs * c.max_seq;
     const size_t vit_rows = c.vit_layers ? (size_t)c.max_envs * p->patches_per_env : 0;
     const size_t flow_rows = c.exp_layers ? (size_t)c.max_envs * (c.chunk + c.frame_tokens) : 0;
-    p->rows_cap = std::max({pre_rows, vit_rows, flow_rows, (size_t)c.max_envs});
+    p->dec_cap = c.max_envs <= 4 ? c.max_envs : (c.max_envs + 7) / 8 * 8;
+    p->rows_cap = std::max({pre_rows, vit_rows, flow_rows, (size_t)p->dec_cap});
     auto wmax = [&](auto f) {
         size_t m = f(p->dec);
         if (c.vit_layers) m = std::max(m, (size_t)f(p->vit));
@@ -934,22 +969,26 @@ int ebrl_policy_create(const ebrl_config* config, uint64_t seed, ebrl_policy** o
         if ((rc = dev_alloc_t(p, &p->vit_bt, vbt.size()))) return bail(rc);
         HIPCHK(p, hipMemcpy(p->vit_bt, vbt.data(), vbt.size() * 4, hipMemcpyHostToDevice));
     }
-    if ((rc = dev_alloc_t(p, &p->h_pre, (size_t)c.max_envs * c.d))) return bail(rc);
-    if ((rc = dev_alloc_t(p, &p->h_norm, (size_t)c.max_envs * c.d))) return bail(rc);
-    HIPCHK(p, hipMemset(p->h_pre, 0, (size_t)c.max_envs * c.d * 4));
-    HIPCHK(p, hipMemset(p->h_norm, 0, (size_t)c.max_envs * c.d * 4));
+    if ((rc = dev_alloc_t(p, &p->h_pre, (size_t)(c.max_envs + 1) * c.d))) return bail(rc);
+    if ((rc = dev_alloc_t(p, &p->h_norm, (size_t)(c.max_envs + 1) * c.d))) return bail(rc);
+    HIPCHK(p, hipMemset(p->h_pre, 0, (size_t)(c.max_envs + 1) * c.d * 4));
+    HIPCHK(p, hipMemset(p->h_norm, 0, (size_t)(c.max_envs + 1) * c.d * 4));
     // split-K workspace: 16 splits of the widest skinny projection
     p->ws_floats = (size_t)16 * 256 * std::max(w_qkv, 2 * w_mlp);
     if ((rc = dev_alloc_t(p, &p->ws, p->ws_floats))) return bail(rc);
     if ((rc = dev_alloc_t(p, &p->counters, ebrl::gemm_counter_words()))) return bail(rc);
     HIPCHK(p, hipMemset(p->counters, 0, ebrl::gemm_counter_words() * 4));
     if (c.action_logits) {
-        if ((rc = dev_alloc_t(p, &p->lg, (size_t)c.max_envs * c.n_bins))) return bail(rc);
-        if ((rc = dev_alloc_t(p, &p->lg_counters, (size_t)c.max_envs))) return bail(rc);
-        HIPCHK(p, hipMemset(p->lg_counters, 0, (size_t)c.max_envs * 4));
+        if ((rc = dev_alloc_t(p, &p->lg, (size_t)p->dec_cap * c.n_bins))) return bail(rc);
+        if ((rc = dev_alloc_t(p, &p->lg_counters, (size_t)p->dec_cap))) return bail(rc);
+        HIPCHK(p, hipMemset(p->lg_counters, 0, (size_t)p->dec_cap * 4));
+        const size_t outs = (size_t)p->dec_cap * c.n_action_tokens;
+        if ((rc = dev_alloc_t(p, &p->dec_tok, outs))) return bail(rc);
+        if ((rc = dev_alloc_t(p, &p->dec_act, outs))) return bail(rc);
+        if ((rc = dev_alloc_t(p, &p->dec_mar, outs))) return bail(rc);
     }
     const int max_splits = (c.max_seq + p->tail + ATTN_DEC_CHUNK - 1) / ATTN_DEC_CHUNK;
-    p->part_floats = (size_t)c.max_envs * c.q_heads * max_splits * (c.head_dim + 2);
+    p->part_floats = (size_t)std::max(c.max_envs, p->dec_cap) * c.q_heads * max_splits * (c.head_dim + 2);
     if ((rc = dev_alloc_t(p, &p->part, p->part_floats))) return bail(rc);
     if (c.exp_layers) {
         const size_t act_rows = (size_t)c.max_envs * c.chunk;
@@ -1035,17 +1074,22 @@ int ebrl_prefill(ebrl_policy* p, const ebrl_obs_batch* obs, const int32_t* env_i
         if (T[i] < 1 || T[i] > c.max_seq)
             return fail(p, EBRL_E_INVALID, "env %d: prefix length %d outside [1, %d]", env_ids[i], T[i], c.max_seq);
     }
-    // ---- KV blocks: release the envs' old caches, then allocate
+    // ---- KV blocks: the budget check counts the blocks these envs already
+    // hold as available (they are replaced), and runs before any env's state
+    // changes, so a call that fails leaves every existing cache intact
+    size_t need = 0, held = 0;
+    for (int i = 0; i < n; ++i) {
+        need += (size_t)(T[i] + p->tail + KV_BLOCK - 1) / KV_BLOCK;
+        held += p->envs[env_ids[i]].blocks.size();
+    }
+    if (need > p->free_blocks.size() + held)
+        return fail(p, EBRL_E_OOM, "KV budget: %zu blocks needed, %zu free", need, p->free_blocks.size() + held);
     for (int i = 0; i < n; ++i) {
         EnvSlot& s = p->envs[env_ids[i]];
         for (int b : s.blocks) p->free_blocks.push_back(b);
         s.blocks.clear();
         s.T = 0;
     }
-    size_t need = 0;
-    for (int i = 0; i < n; ++i) need += (size_t)(T[i] + p->tail + KV_BLOCK - 1) / KV_BLOCK;
-    if (need > p->free_blocks.size())
-        return fail(p, EBRL_E_OOM, "KV budget: %zu blocks needed, %zu free", need, p->free_blocks.size());
     for (int i = 0; i < n; ++i) {
         EnvSlot& s = p->envs[env_ids[i]];
         const int nb = (T[i] + p->tail + KV_BLOCK - 1) / KV_BLOCK;
@@ -1072,7 +1116,6 @@ int ebrl_prefill(ebrl_policy* p, const ebrl_obs_batch* obs, const int32_t* env_i
     // causal tiles late in a sequence see the most keys: dispatch them first
     std::stable_sort(tiles.begin(), tiles.end(),
                      [](const std::pair<int, int>& x, const std::pair<int, int>& y) { return x.second > y.second; });
-    std::stable_sort(tiles.begin(), tiles.end(), [](auto& a, auto& b) { return a.second > b.second; });
     std::vector<int> tile_seq(tiles.size()), tile_q0(tiles.size());
     for (size_t t = 0; t < tiles.size(); ++t) { tile_seq[t] = tiles[t].first; tile_q0[t] = tiles[t].second; }
     std::vector<int> lang_dst, lang_src;
@@ -1176,29 +1219,33 @@ int ebrl_decode_actions(ebrl_policy* p, const int32_t* env_ids, int32_t n, int32
     if (n == 0) return EBRL_OK;
     if (!out_tokens) return fail(p, EBRL_E_INVALID, "out_tokens is NULL");
     const int ntok = c.n_action_tokens, steps = ntok - 1;
-    std::vector<int> seq_env(env_ids, env_ids + n), ident(n);
+    // batch-size class: rows n .. nc-1 decode the padding env; every tile,
+    // split and reduction choice of the kernels depends on the problem shape
+    // only, so the real rows' bits do not depend on the padding
+    const int nc = n <= 4 ? n : std::min(p->dec_cap, (n + 7) / 8 * 8);
+    std::vector<int> seq_env(nc, p->pad_env), ident(nc);
+    std::copy(env_ids, env_ids + n, seq_env.begin());
     std::iota(ident.begin(), ident.end(), 0);
-    int maxT = 0;
-    std::vector<int> kvlen((size_t)std::max(steps, 1) * n), pos((size_t)std::max(steps, 1) * n);
-    for (int i = 0; i < n; ++i) {
-        const int T = p->envs[env_ids[i]].T;
-        maxT = std::max(maxT, T);
+    std::vector<int> kvlen((size_t)std::max(steps, 1) * nc), pos((size_t)std::max(steps, 1) * nc);
+    for (int i = 0; i < nc; ++i) {
+        const int T = p->envs[seq_env[i]].T;
         for (int k = 1; k <= steps; ++k) {
-            kvlen[(size_t)(k - 1) * n + i] = T + k;
-            pos[(size_t)(k - 1) * n + i] = T + k - 1;
+            kvlen[(size_t)(k - 1) * nc + i] = T + k;
+            pos[(size_t)(k - 1) * nc + i] = T + k - 1;
         }
     }
     Meta m;
     const size_t o_env = m.add(seq_env), o_id = m.add(ident), o_kvl = m.add(kvlen), o_pos = m.add(pos);
     int* md = nullptr;
     if ((rc = upload_meta(p, m, false, &md))) return rc;
-    const int max_splits = (maxT + steps + ATTN_DEC_CHUNK - 1) / ATTN_DEC_CHUNK;
+    // split count of the fp32 attention path: the policy's longest sequence
+    const int max_splits = (c.max_seq + steps + ATTN_DEC_CHUNK - 1) / ATTN_DEC_CHUNK;
 
-    const bool fold = fold_decode_norm(p, p->dec, n);
+    const bool fold = fold_decode_norm(p, p->dec, nc);
     auto body = [&]() -> int {
         LogitsArgs la;
-        la.bf16 = p->bf16; la.W = p->w_act; la.d = c.d; la.n_bins = c.n_bins; la.n = n;
-        la.tokens = out_tokens; la.actions = out_actions; la.margins = out_margin; la.ntok = ntok;
+        la.bf16 = p->bf16; la.W = p->w_act; la.d = c.d; la.n_bins = c.n_bins; la.n = nc;
+        la.tokens = p->dec_tok; la.actions = p->dec_act; la.margins = p->dec_mar; la.ntok = ntok;
         la.lg = p->lg; la.counters = p->lg_counters;
         la.X = p->h_pre; la.ldx = c.d; la.rows = md + o_env; la.col = 0;
         prof_begin(p, EBRL_K_OTHER);
@@ -1206,18 +1253,18 @@ int ebrl_decode_actions(ebrl_policy* p, const int32_t* env_ids, int32_t n, int32
         prof_end(p, 0, (double)c.n_bins * c.d * p->esz);
         for (int k = 1; k <= steps; ++k) {
             prof_begin(p, EBRL_K_OTHER);
-            embed_rows(p->bf16, p->e_act, c.n_bins, c.d, out_tokens, nullptr, ntok, k - 1, nullptr, p->X, c.d, n,
+            embed_rows(p->bf16, p->e_act, c.n_bins, c.d, p->dec_tok, nullptr, ntok, k - 1, nullptr, p->X, c.d, nc,
                        p->stream, fold ? p->Xn : nullptr, c.d);
             prof_end(p, 0, 0);
             double kv_bytes = 0;
-            for (int i = 0; i < n; ++i) kv_bytes += (double)(p->envs[env_ids[i]].T + k);
+            for (int i = 0; i < nc; ++i) kv_bytes += (double)(p->envs[seq_env[i]].T + k);
             kv_bytes *= 2.0 * c.kv_heads * c.head_dim * p->esz;
             for (int l = 0; l < c.layers; ++l) {
                 BlockCall b;
-                b.R = p->X; b.rows = n; b.sd = &p->dec; b.w = &p->L_dec[l]; b.kv = dec_kv(p, l);
-                b.seq_env = md + o_env; b.row_seq = md + o_id; b.row_pos = md + o_pos + (size_t)(k - 1) * n;
+                b.R = p->X; b.rows = nc; b.sd = &p->dec; b.w = &p->L_dec[l]; b.kv = dec_kv(p, l);
+                b.seq_env = md + o_env; b.row_seq = md + o_id; b.row_pos = md + o_pos + (size_t)(k - 1) * nc;
                 b.decode = true;
-                b.dec.seq_env = md + o_env; b.dec.kv_len = md + o_kvl + (size_t)(k - 1) * n; b.dec.n = n;
+                b.dec.seq_env = md + o_env; b.dec.kv_len = md + o_kvl + (size_t)(k - 1) * nc; b.dec.n = nc;
                 b.dec.max_splits = max_splits;
                 b.attn_bytes = kv_bytes;
                 b.attn_flop = kv_bytes / p->esz / (2.0 * c.kv_heads * c.head_dim) * 4.0 * c.q_heads * c.head_dim;
@@ -1231,11 +1278,11 @@ int ebrl_decode_actions(ebrl_policy* p, const int32_t* env_ids, int32_t n, int32
         }
         return check_launch(p);
     };
-    const std::vector<uint64_t> key = {1, (uint64_t)n, (uint64_t)max_splits, (uint64_t)(uintptr_t)out_tokens,
-                                       (uint64_t)(uintptr_t)out_actions, (uint64_t)(uintptr_t)out_margin};
+    const std::vector<uint64_t> key = {1, (uint64_t)nc};
     const int inside = (1 << EBRL_K_GEMM_SKINNY) | (1 << EBRL_K_ATTN_DECODE) | (1 << EBRL_K_OTHER) |
-                       (n >= 256 ? (1 << EBRL_K_GEMM) : 0);
+                       (nc >= 256 ? (1 << EBRL_K_GEMM) : 0);
     if ((rc = run_graph(p, key, inside, body))) return rc;
+    copy_decode_out(p->dec_tok, p->dec_act, p->dec_mar, n * ntok, out_tokens, out_actions, out_margin, p->stream);
     return check_launch(p);
 }
 
@@ -1269,6 +1316,10 @@ int ebrl_read_state(ebrl_policy* p, int32_t what, int32_t env_id, int32_t layer,
     case EBRL_STATE_PREFIX_LEN:
         if (bytes < 4) return fail(p, EBRL_E_INVALID, "need 4 bytes");
         *(int32_t*)out = s.T;
+        return EBRL_OK;
+    case EBRL_STATE_GRAPHS:
+        if (bytes < 4) return fail(p, EBRL_E_INVALID, "need 4 bytes");
+        *(int32_t*)out = (int32_t)p->graphs.size();
         return EBRL_OK;
     case EBRL_STATE_H_LAST_PRE:
     case EBRL_STATE_H_LAST: {

@@ -182,6 +182,10 @@ void flow_out(bool bf16, const float* H, int ldh, int rows, int d, const void* W
 
 // Element copy (device) with f32 -> f32.
 void copy_f32(const float* src, float* dst, size_t n, hipStream_t s);
+// The first `count` elements of a decode call's tokens (and, where the
+// destination is not NULL, actions and margins) to the caller's buffers.
+void copy_decode_out(const int* tok, const float* act, const float* mar, int count, int* out_tok, float* out_act,
+                     float* out_mar, hipStream_t s);
 // Standard normals for `rows` rows of per_row floats: Philox4x32-10 with
 // counter (pair, calls[i], env[i], stream) under the seed, Box-Muller.
 void normal_noise(float* out, int rows, int per_row, const int* env, const int* calls, uint64_t seed,

@@ -677,6 +677,23 @@ void copy_f32(const float* src, float* dst, size_t n, hipStream_t s) {
     hipLaunchKernelGGL(copy_f32_kernel, dim3(blocks), dim3(256), 0, s, src, dst, n);
 }
 
+__global__ void copy_decode_out_kernel(const int* tok, const float* act, const float* mar, int count, int* out_tok,
+                                       float* out_act, float* out_mar) {
+    for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < count; i += gridDim.x * blockDim.x) {
+        out_tok[i] = tok[i];
+        if (out_act) out_act[i] = act[i];
+        if (out_mar) out_mar[i] = mar[i];
+    }
+}
+
+void copy_decode_out(const int* tok, const float* act, const float* mar, int count, int* out_tok, float* out_act,
+                     float* out_mar, hipStream_t s) {
+    if (count <= 0) return;
+    const int blocks = std::min((count + 255) / 256, 1024);
+    hipLaunchKernelGGL(copy_decode_out_kernel, dim3(blocks), dim3(256), 0, s, tok, act, mar, count, out_tok, out_act,
+                       out_mar);
+}
+
 
 // ---------------------------------------------------------- seeded noise --
 // Philox4x32-10 (Salmon, Moraes, Dror, Shaw, SC'11), ten rounds of

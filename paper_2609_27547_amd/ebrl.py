@@ -19,7 +19,7 @@ EBRL_OK = 0
 ERRORS = {-1: "EBRL_E_INVALID", -2: "EBRL_E_OOM", -3: "EBRL_E_HIP", -4: "EBRL_E_STATE",
           -5: "EBRL_E_UNSUPPORTED"}
 DTYPE_FP32, DTYPE_BF16 = 0, 1
-STATE_H_LAST_PRE, STATE_H_LAST, STATE_K, STATE_V, STATE_FLOW_V0, STATE_PREFIX_LEN = range(6)
+STATE_H_LAST_PRE, STATE_H_LAST, STATE_K, STATE_V, STATE_FLOW_V0, STATE_PREFIX_LEN, STATE_GRAPHS = range(7)
 K_GEMM, K_GEMM_SKINNY, K_ATTN_PREFILL, K_ATTN_DECODE, K_OTHER = range(5)
 KERNEL_CLASSES = {K_GEMM: "gemm", K_GEMM_SKINNY: "gemm_skinny", K_ATTN_PREFILL: "attn_prefill",
                   K_ATTN_DECODE: "attn_decode", K_OTHER: "other"}
@@ -462,7 +462,7 @@ class Policy:
         c = self.cfg
         if what in (STATE_H_LAST_PRE, STATE_H_LAST):
             out = np.empty(c.d, dtype=np.float32)
-        elif what == STATE_PREFIX_LEN:
+        elif what in (STATE_PREFIX_LEN, STATE_GRAPHS):
             out = np.empty(1, dtype=np.int32)
         elif what == STATE_FLOW_V0:
             out = np.empty((c.chunk, c.adim), dtype=np.float32)

@@ -43,3 +43,26 @@ def check_tokens(gpu_tokens, oracle_result, n_bins=256):
             close += 1
             assert lg[int(t)] >= lg.max() - MARGIN, f"step {k}: token {t} not within margin"
     return close
+
+
+def check_margins(gpu_margins, oracle_result, tol):
+    """The GPU's top-2 margins against the teacher-forced oracle's.  A logit
+    row within `tol` norm-relative of the oracle's moves each logit, and so
+    the gap between two of them, by at most sqrt(2) * tol * ||logits||; the
+    margin of every step is held to that.  Returns the largest deviation in
+    units of that bound."""
+    worst = 0.0
+    for k, m in enumerate(gpu_margins):
+        lg = oracle_result.logits[k]
+        bound = np.sqrt(2.0) * tol * np.linalg.norm(lg)
+        dev = abs(float(m) - float(oracle_result.margins[k]))
+        assert dev <= bound, f"step {k}: margin {m} vs oracle {oracle_result.margins[k]} (bound {bound:.3g})"
+        worst = max(worst, dev / bound)
+    return worst
+
+
+def margin_of(w_act, h_normed):
+    """Top-1 minus top-2 of W_act . h (float64): the margin the action head
+    must report for a final-normed row h."""
+    s = np.sort(np.asarray(w_act, dtype=np.float64) @ np.asarray(h_normed, dtype=np.float64))
+    return float(s[-1] - s[-2])

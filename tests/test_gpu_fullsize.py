@@ -6,20 +6,23 @@ independent, so a sampled env checks the whole batch's code path).
   oracle's teacher-forced single pass.
 * flow-matching expert on the GQA backbone, 64 envs: sampled env's velocity
   at tau = 1 and its denoised chunk.
+* world action model, 64 envs: sampled env's frames, actions and velocity.
 * ragged asynchronous decode on the 7B-class model: a 128-slot pool of
   language-only prefixes (lengths U[200, 320]); calls of random size on the
-  whole GPU and on a CU-masked stream give bitwise identical outputs, and a
-  sampled env matches the oracle.
+  whole GPU and on a CU-masked stream give bitwise identical outputs, and
+  eight sampled envs match the oracle.
 
-Reference: the exact oracle (float64 throughout).  Bound: 2e-2, except where
-rounding to bf16 at the bf16 policy's storage points (GEMM inputs, Q/K/V, P,
-attention and SwiGLU outputs) already moves the exact result further on the
-same input -- measured with the oracle's bf16-emulating mode -- where the
-bound is 1.5 times that deviation.  That happens for the 32-layer decoder on
-a language-only prefix: bf16 rounding flips cascade layer by layer, so any
-bf16-operand implementation lands about that far from the exact result (two
-bf16 implementations differ from each other by a similar amount).  The token
-margin threshold is scaled from the same measurement.
+Reference: the exact oracle (float64 throughout on the stored bf16 weights).
+Bounds: 2e-2 norm-relative for rows, the 1e-2 top-2 margin rule for tokens,
+and margins within what a logit row at the row bound implies -- except for
+the ragged workload's language-only prefixes through the 32-layer decoder.
+There, storing the K/V cache in bf16 (the format the workload fixes) already
+moves the exact result about 2e-2 by layer 31 with every other value kept in
+float64, and rounding the GEMM operands as well about 4e-2 (a CPU table of
+the oracle alone, on the same eight envs, is recorded with the derivation of
+RAGGED_TOL and RAGGED_MARGIN below); no implementation with a bf16 cache and
+bf16 GEMM operands meets 2e-2 on these inputs.  The image prefixes of the
+same model keep the plain bounds.
 """
 import numpy as np
 import pytest
@@ -33,6 +36,15 @@ pytestmark = pytest.mark.gpu
 torch = pytest.importorskip("torch")
 from paper_2609_27547_amd import ebrl as E  # noqa: E402
 
+# Ragged workload (language-only prefixes, 32 layers): rows within 3 x 2e-2,
+# 1.4 x the largest deviation bf16 storage of the cache and the GEMM operands
+# causes in the CPU table (4.3e-2); tokens decided exactly wherever the
+# oracle's top-2 margin exceeds 0.15 (about 2 x the largest t0 logit
+# deviation in that table), otherwise within 0.15 of the oracle's maximum.
+RAGGED_TOL = 6e-2
+RAGGED_MARGIN = 0.15
+RAGGED_SAMPLE = [0, 16, 32, 48, 64, 80, 96, 112]
+
 
 def _dev(a):
     return torch.from_numpy(np.ascontiguousarray(a)).cuda()
@@ -44,51 +56,46 @@ def report(name, value):
 
 @pytest.fixture(scope="module")
 def oracle_7b():
-    exact = M.Policy(M.PRESETS[3], seed=0)
-    emu = M.Policy(M.PRESETS[3], seed=0, emulate_bf16=True)
-    emu._raw = exact._raw           # same generated weights, generated once
-    return exact, emu
+    return M.Policy(M.PRESETS[3], seed=0)
 
 
-def _bound(y_emu, y_exact):
-    return max(P.TOL_BF16, 1.5 * P.row_rel_err(y_emu, y_exact))
-
-
-def _check_prefix(pol, e, st, st_emu, layers, tag):
-    """Returns the hidden-state bound used for this input."""
-    report(f"{tag}.oracle_emulated_vs_exact", P.row_rel_err(st_emu.h_last_pre, st.h_last_pre))
-    bound = _bound(st_emu.h_last_pre, st.h_last_pre)
-    h = pol.read_state(E.STATE_H_LAST_PRE, e)
-    err = P.row_rel_err(h, st.h_last_pre)
-    report(f"{tag}.h_last_pre", err)
-    report(f"{tag}.h_last_pre_vs_emulated", P.row_rel_err(h, st_emu.h_last_pre))
-    assert err < bound
-    hn = pol.read_state(E.STATE_H_LAST, e)
-    assert P.row_rel_err(hn, st.h_last) < _bound(st_emu.h_last, st.h_last)
+def _check_prefix(pol, e, st, layers, tag, tol=P.TOL_BF16):
+    """Last prefix row (pre- and post-norm) and K/V rows of `layers` against
+    the exact oracle; returns the largest deviation."""
+    worst = 0.0
+    checks = [("h_last_pre", pol.read_state(E.STATE_H_LAST_PRE, e), st.h_last_pre),
+              ("h_last", pol.read_state(E.STATE_H_LAST, e), st.h_last)]
     for l in layers:
-        for what, ref, emu in [(E.STATE_K, st.k[l], st_emu.k[l]), (E.STATE_V, st.v[l], st_emu.v[l])]:
+        for what, name, ref in [(E.STATE_K, "k", st.k[l]), (E.STATE_V, "v", st.v[l])]:
             g = P.bf16_to_f64(pol.read_state(what, e, l)).reshape(st.T, -1)
-            ref, emu = ref.reshape(st.T, -1), emu.reshape(st.T, -1)
-            err = P.row_rel_err(g, ref)
-            report(f"{tag}.{'k' if what == E.STATE_K else 'v'}{l}", err)
-            assert err < _bound(emu, ref)
-    return bound
+            checks.append((f"{name}{l}", g, ref.reshape(st.T, -1)))
+    for name, got, ref in checks:
+        err = P.row_rel_err(got, ref)
+        report(f"{tag}.{name}", err)
+        assert err < tol, (tag, name, err)
+        worst = max(worst, err)
+    return worst
 
 
-def _check_tokens(tok, r, r_emu, tag):
-    """Margin rule against the exact oracle; the threshold is 1e-2 or twice
-    the logit deviation that bf16 storage alone causes on this input."""
-    dev = float(np.max(np.abs(r_emu.logits - r.logits)))
-    thr = max(P.MARGIN, 2 * dev)
-    report(f"{tag}.oracle_emulated_logit_dev", dev)
-    close = 0
+def _check_tokens(tok, r, tag, thr=P.MARGIN):
+    """Teacher-forced margin rule at threshold `thr`; returns how many steps
+    the exact-equality branch decided."""
+    strict = 0
     for k, t in enumerate(tok):
         if r.margins[k] > thr:
-            assert int(t) == int(r.tokens[k]), (k, int(t), int(r.tokens[k]), r.margins[k])
+            assert int(t) == int(r.tokens[k]), (tag, k, int(t), int(r.tokens[k]), r.margins[k])
+            strict += 1
         else:
-            close += 1
-            assert r.logits[k][int(t)] >= r.logits[k].max() - thr
-    report(f"{tag}.tokens_decided_within_threshold", close)
+            assert r.logits[k][int(t)] >= r.logits[k].max() - thr, (tag, k)
+    report(f"{tag}.tokens_decided_exactly", strict)
+    return strict
+
+
+def _check_margins(pol, ref, e, mar, r, tag, tol=P.TOL_BF16):
+    w = ref.W("W_act")
+    hg = pol.read_state(E.STATE_H_LAST, e).astype(np.float64)
+    assert abs(float(mar[0]) - P.margin_of(w, hg)) <= 1e-5 * np.linalg.norm(w @ hg)
+    report(f"{tag}.margin_dev_over_bound", P.check_margins(mar, r, tol))
 
 
 def test_7b_vla_full_batch_sampled_env(oracle_7b):
@@ -100,14 +107,12 @@ def test_7b_vla_full_batch_sampled_env(oracle_7b):
     pol.prefill(ids, images=_dev(img), lang_ids=_dev(lang))
     tok, act, mar = pol.decode_actions(ids)
     torch.cuda.synchronize()
-    tok = tok.cpu().numpy()
+    tok, mar = tok.cpu().numpy(), mar.cpu().numpy()
     e = 19
-    exact, emu = oracle_7b
-    st, r = exact.teacher_forced(img[e], lang[e], tok[e, :-1])
-    st2, r2 = emu.teacher_forced(img[e], lang[e], tok[e, :-1])
-    bound = _check_prefix(pol, e, st, st2, [0, 31], "7b")
-    assert bound == P.TOL_BF16          # image prefix: the plain 2e-2 holds
-    _check_tokens(tok[e], r, r2, "7b")
+    st, r = oracle_7b.teacher_forced(img[e], lang[e], tok[e, :-1])
+    _check_prefix(pol, e, st, [0, 31], "7b")
+    _check_tokens(tok[e], r, "7b")
+    _check_margins(pol, oracle_7b, e, mar[e], r, "7b")
     pol.close()
 
 
@@ -123,18 +128,14 @@ def test_flow_expert_full_batch_sampled_env():
     torch.cuda.synchronize()
     out = out.cpu().numpy()
     ref = M.Policy(cfg, seed=0)
-    emu = M.Policy(cfg, seed=0, emulate_bf16=True)
-    emu._raw = ref._raw
     e = 11
-    st, st2 = ref.prefill(img[e], lang[e]), emu.prefill(img[e], lang[e])
-    assert _check_prefix(pol, e, st, st2, [0, 17], "flow") == P.TOL_BF16
+    st = ref.prefill(img[e], lang[e])
+    _check_prefix(pol, e, st, [0, 17], "flow")
     x, v0 = ref.flow_denoise(st, noise[e], return_v0=True)
-    x2, v02 = emu.flow_denoise(st2, noise[e], return_v0=True)
     gv0 = pol.read_state(E.STATE_FLOW_V0, e)
     ev, ex = P.row_rel_err(gv0, v0), P.row_rel_err(out[e], x)
     report("flow.v0", ev)
     report("flow.x10", ex)
-    report("flow.v0_vs_emulated", P.row_rel_err(gv0, v02))
     assert ev < P.TOL_BF16 and ex < P.TOL_BF16
     pol.close()
 
@@ -176,6 +177,7 @@ def balanced_mask(frac_quarters: int, n_cu: int = 256):
     return words
 
 
+@pytest.mark.timeout(1200)
 def test_ragged_decode_partitions_bitwise_and_sampled_parity(oracle_7b):
     cfg = M.PRESETS[3]
     pool = 128
@@ -200,17 +202,25 @@ def test_ragged_decode_partitions_bitwise_and_sampled_parity(oracle_7b):
     finally:
         torch.cuda.synchronize()
         E.destroy_stream(s25)
-    # the same env decoded in another batch composition: bitwise equal
+    # the same env decoded alone and inside another batch: bitwise equal
     ids0 = calls[0]
     e = int(ids0[len(ids0) // 2])
-    tok_solo, _, mar_solo = pol.decode_actions([e])
-    torch.cuda.synchronize()
     j = list(ids0).index(e)
+    tok_solo, _, mar_solo = pol.decode_actions([e])
+    tok_s, _, mar_s = pol.decode_actions(RAGGED_SAMPLE)
+    torch.cuda.synchronize()
     assert torch.equal(tok_solo[0], full[0][0][j]) and torch.equal(mar_solo[0], full[0][1][j])
-    tok_e = full[0][0][j].cpu().numpy()
-    exact, emu = oracle_7b
-    st, r = exact.teacher_forced(None, lang[e][:T[e]], tok_e[:-1])
-    st2, r2 = emu.teacher_forced(None, lang[e][:T[e]], tok_e[:-1])
-    _check_prefix(pol, e, st, st2, [0, 31], "ragged")
-    _check_tokens(tok_e, r, r2, "ragged")
+    if e in RAGGED_SAMPLE:
+        assert torch.equal(tok_s[RAGGED_SAMPLE.index(e)], full[0][0][j])
+    tok_s, mar_s = tok_s.cpu().numpy(), mar_s.cpu().numpy()
+    strict, rows_within_plain = 0, 0
+    for i, e in enumerate(RAGGED_SAMPLE):
+        st, r = oracle_7b.teacher_forced(None, lang[e][:T[e]], tok_s[i, :-1])
+        worst = _check_prefix(pol, e, st, [0, 31], f"ragged{e}", tol=RAGGED_TOL)
+        rows_within_plain += worst < P.TOL_BF16
+        strict += _check_tokens(tok_s[i], r, f"ragged{e}", thr=RAGGED_MARGIN)
+        _check_margins(pol, oracle_7b, e, mar_s[i], r, f"ragged{e}", tol=RAGGED_TOL)
+    print(f"RAGGED tokens decided exactly: {strict} of {7 * len(RAGGED_SAMPLE)}; "
+          f"envs with every row within 2e-2: {rows_within_plain} of {len(RAGGED_SAMPLE)}", flush=True)
+    assert 2 * strict > 7 * len(RAGGED_SAMPLE)   # most tokens decided by equality
     pol.close()

@@ -28,6 +28,16 @@ def _obs(cfg, ids, seed):
     return img, lang
 
 
+def _check_margins(pol, ref, e, mar, r, tol):
+    """The reported margins: step 0 exactly that of the GPU's own final-normed
+    last prefix row (float32 arithmetic on both sides of the same row), every
+    step within the bound a logit row at `tol` implies (tests/parity.py)."""
+    w = ref.W("W_act")
+    hg = pol.read_state(E.STATE_H_LAST, e).astype(np.float64)
+    assert abs(float(mar[0]) - P.margin_of(w, hg)) <= 1e-5 * np.linalg.norm(w @ hg)
+    return P.check_margins(mar, r, tol)
+
+
 def _ebrl_config(o: M.Config, max_envs: int, max_seq: int = 0) -> "E.Config":
     c = E.Config()
     c.dtype = E.DTYPE_BF16 if o.bf16 else E.DTYPE_FP32
@@ -151,7 +161,7 @@ def test_tiny_fp32_end_to_end(tiny):
     pol.prefill(ids, images=_dev(img), lang_ids=_dev(lang))
     tok, act, mar = pol.decode_actions(ids)
     torch.cuda.synchronize()
-    tok, act = tok.cpu().numpy(), act.cpu().numpy()
+    tok, act, mar = tok.cpu().numpy(), act.cpu().numpy(), mar.cpu().numpy()
     for i, e in enumerate(ids):
         st = states[i]
         assert P.row_rel_err(pol.read_state(E.STATE_H_LAST_PRE, e), st.h_last_pre) < P.TOL_FP32
@@ -163,6 +173,7 @@ def test_tiny_fp32_end_to_end(tiny):
             assert P.row_rel_err(v.reshape(st.T, -1), st.v[l].reshape(st.T, -1)) < P.TOL_FP32
         r = ref.decode(st, forced=tok[i, :-1])
         P.check_tokens(tok[i], r)
+        _check_margins(pol, ref, e, mar[i], r, P.TOL_FP32)
         assert np.array_equal(act[i], (-1 + (2 * tok[i].astype(np.float64) + 1) / 256).astype(np.float32))
     pol.close()
 
@@ -229,6 +240,66 @@ def test_abi_errors():
     pol.close()
 
 
+def test_kv_budget_oom_keeps_caches_and_reprefill(tiny):
+    """A KV budget of 6 blocks holds three tiny envs (2 blocks each).  A
+    prefill that needs more fails with EBRL_E_OOM and leaves every existing
+    cache as it was (decode still gives the same bits, and the oracle's
+    answer); re-prefilling an env with new inputs reuses its own blocks and
+    matches the oracle on the new prefix, the other envs unchanged."""
+    cfg, ids, img, lang, ref, states = tiny
+    block_bytes = 2 * cfg.kv_heads * 16 * cfg.head_dim * 4 * cfg.layers
+    pol = E.Policy(1, seed=0, kv_budget_bytes=6 * block_bytes)
+    three = [0, 1, 2]
+    pol.prefill(three, images=_dev(img[three]), lang_ids=_dev(lang[three]))
+    tok0, act0, mar0 = pol.decode_actions(three)
+    torch.cuda.synchronize()
+    for bad in ([3], [0, 3]):
+        with pytest.raises(E.EbrlError) as ex:
+            pol.prefill(bad, images=_dev(img[bad]), lang_ids=_dev(lang[bad]))
+        assert ex.value.code == -2
+        tok1, act1, mar1 = pol.decode_actions(three)
+        torch.cuda.synchronize()
+        assert torch.equal(tok1, tok0) and torch.equal(act1, act0) and torch.equal(mar1, mar0)
+        assert int(pol.read_state(E.STATE_PREFIX_LEN, 3)[0]) == 0
+    tok0 = tok0.cpu().numpy()
+    for e in three:
+        P.check_tokens(tok0[e], ref.decode(states[e], forced=tok0[e, :-1]))
+    # env 1 re-prefilled with env 5's observation
+    pol.prefill([1], images=_dev(img[[5]]), lang_ids=_dev(lang[[5]]))
+    tok2, _, _ = pol.decode_actions(three)
+    torch.cuda.synchronize()
+    tok2 = tok2.cpu().numpy()
+    st5 = states[5]
+    assert P.row_rel_err(pol.read_state(E.STATE_H_LAST_PRE, 1), st5.h_last_pre) < P.TOL_FP32
+    k = pol.read_state(E.STATE_K, 1, 1)
+    assert P.row_rel_err(k.reshape(st5.T, -1), st5.k[1].reshape(st5.T, -1)) < P.TOL_FP32
+    P.check_tokens(tok2[1], ref.decode(st5, forced=tok2[1, :-1]))
+    assert np.array_equal(tok2[[0, 2]], tok0[[0, 2]])
+    pol.close()
+
+
+def test_decode_graphs_per_size_class_not_per_output_buffer(tiny):
+    """Decode graphs are captured once per batch-size class (n up to 4, then
+    multiples of 8) and never for new output buffers; rows padded up to the
+    class do not change the real rows' bits."""
+    cfg, ids, img, lang, ref, states = tiny
+    pol = E.Policy(1, seed=0)
+    pol.prefill(ids, images=_dev(img), lang_ids=_dev(lang))
+    graphs = lambda: int(pol.read_state(E.STATE_GRAPHS, 0)[0])
+    tok8, act8, mar8 = pol.decode_actions(ids)
+    assert graphs() == 1
+    for n in (5, 6, 7, 8, 5):                       # one class: n in 5..8
+        tok, act, mar = pol.decode_actions(ids[:n])  # fresh outputs every call
+        torch.cuda.synchronize()
+        assert torch.equal(tok, tok8[:n]) and torch.equal(act, act8[:n]) and torch.equal(mar, mar8[:n])
+    assert graphs() == 1
+    tok3, _, _ = pol.decode_actions([6, 1, 3])
+    torch.cuda.synchronize()
+    assert graphs() == 2
+    assert torch.equal(tok3, tok8[[6, 1, 3]])
+    pol.close()
+
+
 # ---------------------------------------------------- small bf16 model --
 
 @pytest.fixture(scope="module")
@@ -241,13 +312,13 @@ def small():
     tok, act, mar = pol.decode_actions(ids)
     torch.cuda.synchronize()
     ref = M.Policy(cfg, seed=0)
-    yield cfg, ids, img, lang, pol, tok.cpu().numpy(), ref
+    yield cfg, ids, img, lang, pol, tok.cpu().numpy(), ref, mar.cpu().numpy()
     pol.close()
 
 
 @pytest.mark.parametrize("env", [0, 37, 63])
 def test_small_bf16_sampled_envs(small, env):
-    cfg, ids, img, lang, pol, tok, ref = small
+    cfg, ids, img, lang, pol, tok, ref, mar = small
     st = ref.prefill(img[env], lang[env])
     assert P.row_rel_err(pol.read_state(E.STATE_H_LAST_PRE, env), st.h_last_pre) < P.TOL_BF16
     assert P.row_rel_err(pol.read_state(E.STATE_H_LAST, env), st.h_last) < P.TOL_BF16
@@ -256,7 +327,9 @@ def test_small_bf16_sampled_envs(small, env):
         v = P.bf16_to_f64(pol.read_state(E.STATE_V, env, l))
         assert P.row_rel_err(k.reshape(st.T, -1), st.k[l].reshape(st.T, -1)) < P.TOL_BF16
         assert P.row_rel_err(v.reshape(st.T, -1), st.v[l].reshape(st.T, -1)) < P.TOL_BF16
-    P.check_tokens(tok[env], ref.decode(st, forced=tok[env, :-1]))
+    r = ref.decode(st, forced=tok[env, :-1])
+    P.check_tokens(tok[env], r)
+    _check_margins(pol, ref, env, mar[env], r, P.TOL_BF16)
 
 
 def _half_masks():
@@ -274,7 +347,7 @@ def test_small_bf16_decode_bitwise_beside_gemm_load(small):
     # stand-in) keep the other half busy: outputs bitwise equal to the run on
     # the whole GPU -- no tile, split or reduction choice depends on the CUs
     # available or on timing
-    cfg, ids, img, lang, pol, tok, ref = small
+    cfg, ids, img, lang, pol, tok, ref, _ = small
     tok_f, act_f, mar_f = pol.decode_actions(ids)
     torch.cuda.synchronize()
     gmask, lmask = _half_masks()
@@ -458,16 +531,18 @@ def test_tiny_vit_bf16_parity():
     img, lang = _obs(o, ids, 1003)
     pol = E.Policy(_ebrl_config(o, 2), seed=0)
     pol.prefill(ids, images=_dev(img), lang_ids=_dev(lang))
-    tok, _, _ = pol.decode_actions(ids)
+    tok, _, mar = pol.decode_actions(ids)
     torch.cuda.synchronize()
-    tok = tok.cpu().numpy()
+    tok, mar = tok.cpu().numpy(), mar.cpu().numpy()
     ref = M.Policy(o, seed=0)
     for i, e in enumerate(ids):
         st = ref.prefill(img[i], lang[i])
         assert P.row_rel_err(pol.read_state(E.STATE_H_LAST_PRE, e), st.h_last_pre) < P.TOL_BF16
         k = P.bf16_to_f64(pol.read_state(E.STATE_K, e, 0))
         assert P.row_rel_err(k.reshape(st.T, -1), st.k[0].reshape(st.T, -1)) < P.TOL_BF16
-        P.check_tokens(tok[i], ref.decode(st, forced=tok[i, :-1]))
+        r = ref.decode(st, forced=tok[i, :-1])
+        P.check_tokens(tok[i], r)
+        _check_margins(pol, ref, e, mar[i], r, P.TOL_BF16)
     pol.close()
 
 
@@ -519,9 +594,9 @@ def test_bf16_attention_at_block_and_tile_boundaries(hd):
     _, lang = _obs(o, ids, 1008)
     pol = E.Policy(_ebrl_config(o, len(ids)), seed=0)
     pol.prefill(ids, images=None, lang_ids=_dev(lang), lang_len=lens)
-    tok, _, _ = pol.decode_actions(ids)
+    tok, _, mar = pol.decode_actions(ids)
     torch.cuda.synchronize()
-    tok = tok.cpu().numpy()
+    tok, mar = tok.cpu().numpy(), mar.cpu().numpy()
     ref = M.Policy(o, seed=0)
     for e, T in zip(ids, lens):
         st = ref.prefill(None, lang[e][:T])
@@ -529,7 +604,9 @@ def test_bf16_attention_at_block_and_tile_boundaries(hd):
         assert P.row_rel_err(pol.read_state(E.STATE_H_LAST_PRE, e), st.h_last_pre) < P.TOL_BF16
         k = P.bf16_to_f64(pol.read_state(E.STATE_K, e, 1))
         assert P.row_rel_err(k.reshape(T, -1), st.k[1].reshape(T, -1)) < P.TOL_BF16
-        P.check_tokens(tok[e], ref.decode(st, forced=tok[e, :-1]))
+        r = ref.decode(st, forced=tok[e, :-1])
+        P.check_tokens(tok[e], r)
+        _check_margins(pol, ref, e, mar[e], r, P.TOL_BF16)
     pol.close()
 
 
