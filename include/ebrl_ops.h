@@ -18,7 +18,10 @@ extern "C" {
  * path, fp32 accumulate); EBRL_DTYPE_FP32: float32.  C is float32 row-major
  * with leading dimension N.  Requires M, N >= 1, K >= 8 and K % 8 == 0;
  * the kernel choice (tile, split over K) depends only on (M, N, K).
- * stream: hipStream_t or NULL. */
+ * stream: hipStream_t or NULL.  K splits (M < 256) write their partial sums
+ * to a workspace the library allocates on the first call per (device,
+ * stream) and keeps until the process ends, so calls on different streams
+ * may overlap.  Returns EBRL_E_OOM if that allocation fails. */
 int ebrl_op_gemm(int32_t dtype, const void* A, const void* B, float* C, int32_t M, int32_t N,
                  int32_t K, void* stream);
 

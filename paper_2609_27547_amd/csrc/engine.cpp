@@ -1429,10 +1429,12 @@ int ebrl_profile_read(ebrl_policy* p, int32_t cls, int64_t* launches, double* to
 
 // ------------------------------------------------------------- ops ABI --
 
+// Split-K workspace of ebrl_op_gemm: one per (device, stream handle), so
+// calls on different streams never share partial sums or tile counters.
+// 64 MB of partials plus the counters each, kept for the process lifetime.
+static constexpr size_t OP_WS_FLOATS = (size_t)16 << 20;
 static std::mutex g_ws_mu;
-static float* g_ws = nullptr;
-static size_t g_ws_floats = 0;
-static int g_ws_dev = -1;
+static std::map<std::pair<int, uintptr_t>, float*> g_ws;
 
 int ebrl_op_stream_read(const void* buf, int64_t bytes, uint32_t* out, void* stream) {
     if (!buf || !out || bytes < 16 || bytes % 16 || (uintptr_t)buf % 16) return EBRL_E_INVALID;
@@ -1444,22 +1446,24 @@ int ebrl_op_gemm(int32_t dtype, const void* A, const void* B, float* C, int32_t 
                  void* stream) {
     if (!A || !B || !C || M < 1 || N < 1 || K < 8 || K % 8 || N % 4) return EBRL_E_INVALID;
     if (dtype != EBRL_DTYPE_BF16 && dtype != EBRL_DTYPE_FP32) return EBRL_E_INVALID;
-    std::lock_guard<std::mutex> lk(g_ws_mu);
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess) return EBRL_E_HIP;
-    if (!g_ws || g_ws_dev != dev) {
-        // 64 MB of partials plus the tile counters, kept for the process lifetime
-        g_ws_floats = (size_t)16 << 20;
-        const size_t words = g_ws_floats + ebrl::gemm_counter_words();
-        if (hipMalloc((void**)&g_ws, words * 4) != hipSuccess) { g_ws = nullptr; return EBRL_E_OOM; }
-        if (hipMemset(g_ws + g_ws_floats, 0, ebrl::gemm_counter_words() * 4) != hipSuccess) return EBRL_E_HIP;
-        g_ws_dev = dev;
+    float* ws = nullptr;
+    {
+        std::lock_guard<std::mutex> lk(g_ws_mu);
+        float*& slot = g_ws[{dev, (uintptr_t)stream}];
+        if (!slot) {
+            const size_t words = OP_WS_FLOATS + ebrl::gemm_counter_words();
+            if (hipMalloc((void**)&slot, words * 4) != hipSuccess) { slot = nullptr; return EBRL_E_OOM; }
+            if (hipMemset(slot + OP_WS_FLOATS, 0, ebrl::gemm_counter_words() * 4) != hipSuccess) return EBRL_E_HIP;
+        }
+        ws = slot;
     }
     GemmArgs a;
     a.bf16 = dtype == EBRL_DTYPE_BF16;
     a.A = A; a.lda = K; a.B = B; a.ldb = K; a.M = M; a.N = N; a.K = K;
-    a.epi = EPI_F32; a.C = C; a.ldc = N; a.ws = g_ws; a.ws_floats = g_ws_floats;
-    a.counters = reinterpret_cast<unsigned*>(g_ws + g_ws_floats);
+    a.epi = EPI_F32; a.C = C; a.ldc = N; a.ws = ws; a.ws_floats = OP_WS_FLOATS;
+    a.counters = reinterpret_cast<unsigned*>(ws + OP_WS_FLOATS);
     a.split_ok = M < 256;
     ebrl::gemm(a, (hipStream_t)stream);
     return hipGetLastError() == hipSuccess ? EBRL_OK : EBRL_E_HIP;

@@ -16,6 +16,20 @@ Two modes:
       and writes profiles/traffic_<W>.json (read by bench.py).
       The JSON records a hash of the GEMM sources: bench.py reports the
       traffic only while the kernel is unchanged since the counters were taken.
+
+  python3 pmc_traffic.py kstats --dir D --title T --command C --out F.md
+      Per-kernel table (calls, total, average, share) of a rocprofv3
+      --kernel-trace run, plus family averages of the large-M GEMM (every
+      launch, as bench.py's GEMM class counts them), the decode GEMM and the
+      attention kernels.
+
+  python3 pmc_traffic.py counters --dir D [--dir D2 ...] --kernel K [--kernel K2 ...]
+          --title T --command C --out F.md [--copy-fetch D --copy-write D]
+      Per-dispatch averages of every counter found under the run dirs for
+      the kernels whose names contain K; MfmaUtil is reported as is (percent
+      of the MFMA pipes' cycles busy over the dispatch), FETCH_SIZE and
+      WRITE_SIZE (KiB) also in bytes scaled by the 1 GiB copy when its two
+      calibration runs are given.
 """
 from __future__ import annotations
 
@@ -71,6 +85,118 @@ def _per_dispatch(d: str, counter: str, name_part: str):
     return list(vals.values())
 
 
+def _all_counters(d: str):
+    """{(kernel name, counter): [per-dispatch values]} from rocprofv3 output under d."""
+    import sqlite3
+    out = {}
+    for db in glob.glob(os.path.join(d, "**", "*results.db"), recursive=True):
+        cur = sqlite3.connect(db).cursor()
+        seen = {}
+        for pid, disp, name, cname, value in cur.execute(
+                "select pid, dispatch_id, kernel_name, counter_name, value from counters_collection"):
+            seen[(db, pid, disp, cname)] = (name, cname, float(value))
+        for name, cname, value in seen.values():
+            out.setdefault((name, cname), []).append(value)
+    for f in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
+        with open(f, newline="") as fh:
+            for r in csv.DictReader(fh):
+                out.setdefault((r["Kernel_Name"], r["Counter_Name"]), []).append(float(r["Counter_Value"]))
+    return out
+
+
+def _dispatches(d: str):
+    """[(kernel name, duration ns)] of every dispatch in a --kernel-trace run under d."""
+    import sqlite3
+    rows = []
+    for db in glob.glob(os.path.join(d, "**", "*results.db"), recursive=True):
+        cur = sqlite3.connect(db).cursor()
+        rows += [(n, float(du)) for n, du in cur.execute("select name, duration from kernels")]
+    for f in glob.glob(os.path.join(d, "**", "*kernel_trace.csv"), recursive=True):
+        with open(f, newline="") as fh:
+            for r in csv.DictReader(fh):
+                rows.append((r["Kernel_Name"], float(r["End_Timestamp"]) - float(r["Start_Timestamp"])))
+    if not rows:
+        sys.exit(f"no kernel trace under {d}")
+    return rows
+
+
+def kstats_main(args):
+    rows = _dispatches(args.dir)
+    per = {}
+    for n, du in rows:
+        c, t = per.get(n, (0, 0.0))
+        per[n] = (c + 1, t + du)
+    total = sum(t for _, t in per.values())
+    lines = [f"# {args.title}", "", "Command (repository root on the GPU host; `cd /tmp && export TMPDIR=/tmp` first):",
+             "", "```", args.command, "```", "",
+             f"Total kernel time {total / 1e6:.1f} ms over {len(rows)} dispatches.", ""]
+    fams = [("gemm_bf16_big_kernel (all epilogues: the bench's large-M GEMM class)",
+             lambda n: "gemm_bf16_big_kernel" in n),
+            ("gemm_bf16_decode_kernel (all epilogues)", lambda n: "gemm_bf16_decode_kernel" in n),
+            ("attn_prefill_bf16_kernel", lambda n: "attn_prefill_bf16_kernel" in n),
+            ("attn_decode_bf16_kernel", lambda n: "attn_decode" in n)]
+    for title, pred in fams:
+        c = sum(v[0] for n, v in per.items() if pred(n))
+        t = sum(v[1] for n, v in per.items() if pred(n))
+        if c:
+            lines.append(f"Family `{title}`: {c} dispatches, average {t / c / 1e3:.2f} us, "
+                         f"{100 * t / total:.1f} % of kernel time.")
+            lines.append("")
+    lines += ["| kernel | calls | total (us) | average (us) | % |", "|---|---:|---:|---:|---:|"]
+    for n, (c, t) in sorted(per.items(), key=lambda kv: -kv[1][1]):
+        if 100 * t / total < 0.01:
+            continue
+        lines.append(f"| `{_short(n)}` | {c} | {t / 1e3:.0f} | {t / c / 1e3:.2f} | {100 * t / total:.2f} |")
+    _write(args.out, lines)
+
+
+def counters_main(args):
+    vals = {}
+    for d in args.dir:
+        for k, v in _all_counters(d).items():
+            vals.setdefault(k, []).extend(v)
+    scale = {}
+    if args.copy_fetch and args.copy_write:
+        cf = sorted(_per_dispatch(args.copy_fetch, "FETCH_SIZE", "copyBuffer"))
+        cw = sorted(_per_dispatch(args.copy_write, "WRITE_SIZE", "copyBuffer"))
+        scale = {"FETCH_SIZE": COPY_BYTES / (cf[len(cf) // 2] * 1024.0),
+                 "WRITE_SIZE": COPY_BYTES / (cw[len(cw) // 2] * 1024.0)}
+    lines = [f"# {args.title}", "", "Commands (repository root on the GPU host; `cd /tmp && export TMPDIR=/tmp` "
+             "first; one rocprofv3 run per counter set):", "", "```", args.command, "```", ""]
+    if scale:
+        lines += [f"Calibration: a 1 GiB device copy reads FETCH_SIZE x {scale['FETCH_SIZE']:.3f} and "
+                  f"WRITE_SIZE x {scale['WRITE_SIZE']:.3f} bytes per KiB counted.", ""]
+    lines += ["| kernel | counter | dispatches | average per dispatch | scaled bytes per dispatch |",
+              "|---|---|---:|---:|---:|"]
+    for kpat in args.kernel:
+        for (name, cname), v in sorted(vals.items()):
+            if kpat not in name:
+                continue
+            avg = sum(v) / len(v)
+            sb = f"{avg * 1024.0 * scale[cname] / 1e6:.2f} MB" if cname in scale else ""
+            lines.append(f"| `{_short(name)}` | {cname} | {len(v)} | {avg:.4g} | {sb} |")
+    _write(args.out, lines)
+
+
+def _short(name: str) -> str:
+    """Kernel name without its parameter list."""
+    depth = 0
+    for i, ch in enumerate(name):
+        if ch == "<":
+            depth += 1
+        elif ch == ">":
+            depth -= 1
+        elif ch == "(" and depth == 0:
+            return name[:i]
+    return name
+
+
+def _write(path, lines):
+    with open(path, "w") as f:
+        f.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
 def copy_main():
     import torch
     n = COPY_BYTES // 4
@@ -121,6 +247,16 @@ def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     sub = ap.add_subparsers(dest="mode", required=True)
     sub.add_parser("copy")
+    k = sub.add_parser("kstats")
+    for a in ["dir", "title", "command", "out"]:
+        k.add_argument(f"--{a}", required=True)
+    c = sub.add_parser("counters")
+    c.add_argument("--dir", action="append", required=True)
+    c.add_argument("--kernel", action="append", required=True)
+    for a in ["title", "command", "out"]:
+        c.add_argument(f"--{a}", required=True)
+    c.add_argument("--copy-fetch")
+    c.add_argument("--copy-write")
     s = sub.add_parser("summarize")
     for k in ["copy-fetch", "copy-write", "fetch", "write", "kernel", "workload"]:
         s.add_argument(f"--{k}", required=True)
@@ -128,6 +264,10 @@ def main():
     args = ap.parse_args()
     if args.mode == "copy":
         copy_main()
+    elif args.mode == "kstats":
+        kstats_main(args)
+    elif args.mode == "counters":
+        counters_main(args)
     else:
         summarize_main(args)
 
