@@ -25,6 +25,23 @@ extern "C" {
 int ebrl_op_gemm(int32_t dtype, const void* A, const void* B, float* C, int32_t M, int32_t N,
                  int32_t K, void* stream);
 
+/* For callers that cannot allocate device memory: code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc.  The same
+ * product as ebrl_op_gemm, bit for bit (same kernels and the same tile and
+ * split choice), except that the partial sums and tile counters of a K split
+ * live in a fixed device array of EBRL_OP_GEMM_NOALLOC_SCRATCH_BYTES that
+ * each GPU the library runs on holds until the process ends; the call
+ * allocates nothing and issues no memset.  Shapes whose split would write
+ * more partial sums than the array holds return EBRL_E_INVALID (without a
+ * split, e.g. M >= 256, any shape is accepted).  Every call on one GPU shares
+ * that GPU's array: calls that overlap in time on one GPU (on different
+ * streams or from different host threads) race and give wrong results;
+ * calls ordered on one stream do not.  Same arguments and errors as
+ * ebrl_op_gemm otherwise. */
+#define EBRL_OP_GEMM_NOALLOC_SCRATCH_BYTES ((int64_t)16 * 1024 * 1024 + 4096 * 4)
+int ebrl_op_gemm_noalloc(int32_t dtype, const void* A, const void* B, float* C, int32_t M, int32_t N,
+                         int32_t K, void* stream);
+
 /* Reads `bytes` of device memory at `buf` once with non-temporal 16-byte
  * loads (each workgroup a contiguous range).  Every loaded word feeds an XOR
  * that decides whether *out (device, 4 bytes) is written, so no load can be

@@ -1469,4 +1469,59 @@ int ebrl_op_gemm(int32_t dtype, const void* A, const void* B, float* C, int32_t 
     return hipGetLastError() == hipSuccess ? EBRL_OK : EBRL_E_HIP;
 }
 
+// ebrl_op_gemm_noalloc: the same product with its split-K partials and tile
+// counters in `scratch`, a fixed device array each GPU holds for the whole
+// process, instead of memory the library allocates.  The array's name in
+// host code is not a device address: its address on each device comes from
+// hipGetSymbolAddress, taken once per device with that device current.
+// The counters start at zero (device globals are zero-initialised) and
+// every kernel that uses one leaves it at zero.
+static constexpr size_t NOALLOC_WS_FLOATS = (size_t)4 << 20;   // 16 MB of partial sums
+static constexpr size_t NOALLOC_COUNTER_WORDS = 4096;          // = gemm_counter_words()
+static __device__ __align__(256) float scratch[NOALLOC_WS_FLOATS + NOALLOC_COUNTER_WORDS];
+static constexpr int NOALLOC_MAX_DEVICES = 64;
+static std::mutex g_scratch_mu;
+static float* g_scratch_ptr[NOALLOC_MAX_DEVICES];
+
+static int scratch_on_device(int dev, float** out) {
+    if (dev < 0 || dev >= NOALLOC_MAX_DEVICES) return EBRL_E_INVALID;
+    std::lock_guard<std::mutex> lk(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void* ptr = nullptr;
+        if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr) {
+            (void)hipGetLastError();
+            return EBRL_E_HIP;
+        }
+        g_scratch_ptr[dev] = static_cast<float*>(ptr);
+    }
+    *out = g_scratch_ptr[dev];
+    return EBRL_OK;
+}
+
+int ebrl_op_gemm_noalloc(int32_t dtype, const void* A, const void* B, float* C, int32_t M, int32_t N, int32_t K,
+                         void* stream) {
+    static_assert(NOALLOC_COUNTER_WORDS >= 4096, "tile counters of the decode GEMM");
+    if (!A || !B || !C || M < 1 || N < 1 || K < 8 || K % 8 || N % 4) return EBRL_E_INVALID;
+    if (dtype != EBRL_DTYPE_BF16 && dtype != EBRL_DTYPE_FP32) return EBRL_E_INVALID;
+    if (ebrl::gemm_counter_words() > NOALLOC_COUNTER_WORDS) return EBRL_E_INVALID;
+    const bool bf16 = dtype == EBRL_DTYPE_BF16;
+    // plan exactly as ebrl_op_gemm does (same workspace size), so both give
+    // the same bits; shapes whose plan writes more partials than fit are refused
+    const bool split_ok = M < 256;
+    if (ebrl::gemm_ws_floats_used(bf16, M, N, K, OP_WS_FLOATS, split_ok) > NOALLOC_WS_FLOATS) return EBRL_E_INVALID;
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return EBRL_E_HIP;
+    float* ws = nullptr;
+    const int rc = scratch_on_device(dev, &ws);
+    if (rc) return rc;
+    GemmArgs a;
+    a.bf16 = bf16;
+    a.A = A; a.lda = K; a.B = B; a.ldb = K; a.M = M; a.N = N; a.K = K;
+    a.epi = EPI_F32; a.C = C; a.ldc = N; a.ws = ws; a.ws_floats = OP_WS_FLOATS;
+    a.counters = reinterpret_cast<unsigned*>(ws + NOALLOC_WS_FLOATS);
+    a.split_ok = split_ok;
+    ebrl::gemm(a, (hipStream_t)stream);
+    return hipGetLastError() == hipSuccess ? EBRL_OK : EBRL_E_HIP;
+}
+
 }  // extern "C"

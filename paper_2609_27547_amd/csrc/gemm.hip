@@ -1139,4 +1139,11 @@ size_t gemm_counter_words() {
     return DEC_MAX_COUNTERS;
 }
 
+size_t gemm_ws_floats_used(bool bf16, int M, int N, int K, size_t ws_floats, bool split_ok) {
+    const GemmPlan p = plan_gemm(bf16, M, N, K, ws_floats, split_ok && M <= SPLIT_MAX_M);
+    if (p.splits <= 1) return 0;
+    if (p.dec) return (size_t)((N + p.dbn - 1) / p.dbn) * p.m_tiles * p.splits * DEC_TILE_FLOATS;
+    return (size_t)p.splits * M * N;
+}
+
 }  // namespace ebrl

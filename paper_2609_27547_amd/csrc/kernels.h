@@ -53,6 +53,8 @@ int gemm(const GemmArgs& a, hipStream_t s);
 int gemm_splits(bool bf16, int M, int N, int K, size_t ws_floats, bool split_ok);
 bool gemm_row_norm_ok(bool bf16, int M, int N, int K, size_t ws_floats);
 size_t gemm_counter_words();
+// Workspace floats the plan for (M, N, K) writes (0 without a K split).
+size_t gemm_ws_floats_used(bool bf16, int M, int N, int K, size_t ws_floats, bool split_ok);
 
 // ------------------------------------------------------------- attention --
 // Paged KV: layer base pointer; physical block b holds

@@ -82,7 +82,7 @@ EXPORTED = [
     "ebrl_stream_create_cu_masked", "ebrl_stream_destroy", "ebrl_policy_bind_stream",
     "ebrl_prefill", "ebrl_decode_actions", "ebrl_flow_denoise", "ebrl_wam_denoise", "ebrl_last_error",
     "ebrl_read_state", "ebrl_generate_weight_host", "ebrl_read_weight", "ebrl_write_weight",
-    "ebrl_profile_enable", "ebrl_profile_read", "ebrl_op_gemm", "ebrl_op_stream_read",
+    "ebrl_profile_enable", "ebrl_profile_read", "ebrl_op_gemm", "ebrl_op_gemm_noalloc", "ebrl_op_stream_read",
     "ebrl_alloc_solve", "ebrl_alloc_objective", "ebrl_alloc_monitor_create", "ebrl_alloc_monitor_observe",
     "ebrl_alloc_monitor_destroy", "ebrl_alloc_refine",
     "ebrl_sched_create", "ebrl_sched_destroy", "ebrl_sched_dispatch", "ebrl_sched_complete",
@@ -121,6 +121,7 @@ def lib():
         "ebrl_profile_read": (i32, [vp, i32, ctypes.POINTER(i64), ctypes.POINTER(ctypes.c_double),
                                     ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double), i32]),
         "ebrl_op_gemm": (i32, [i32, vp, vp, vp, i32, i32, i32, vp]),
+        "ebrl_op_gemm_noalloc": (i32, [i32, vp, vp, vp, i32, i32, i32, vp]),
         "ebrl_op_stream_read": (i32, [vp, i64, vp, vp]),
         "ebrl_alloc_solve": (i32, [ctypes.POINTER(AllocProfiles), ctypes.POINTER(AllocLimits),
                                    ctypes.POINTER(AllocResult)]),
@@ -325,16 +326,18 @@ def generate_weight_host(seed: int, tensor_id: int, count: int, std: float, bf16
     return out
 
 
-def op_gemm(A, B, C, stream=None) -> None:
-    """C = A B^T through the library's GEMM kernel (torch device tensors)."""
+def op_gemm(A, B, C, stream=None, noalloc=False) -> None:
+    """C = A B^T through the library's GEMM kernel (torch device tensors);
+    noalloc: the entry point that allocates nothing (fixed device scratch)."""
     import torch
     dt = DTYPE_BF16 if A.dtype == torch.bfloat16 else DTYPE_FP32
     M, K = A.shape
     N = B.shape[0]
     s = stream if stream is not None else torch.cuda.current_stream().cuda_stream
-    rc = lib().ebrl_op_gemm(dt, A.data_ptr(), B.data_ptr(), C.data_ptr(), M, N, K, s)
+    fn = lib().ebrl_op_gemm_noalloc if noalloc else lib().ebrl_op_gemm
+    rc = fn(dt, A.data_ptr(), B.data_ptr(), C.data_ptr(), M, N, K, s)
     if rc != EBRL_OK:
-        raise EbrlError(rc, "ebrl_op_gemm")
+        raise EbrlError(rc, "ebrl_op_gemm_noalloc" if noalloc else "ebrl_op_gemm")
 
 
 def op_stream_read(buf, out, stream=None) -> None:
