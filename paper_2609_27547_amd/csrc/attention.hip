@@ -15,9 +15,10 @@
 //   sum taken before rounding.
 // attn_prefill_f32: plain per-(query, head) kernel for fp32 policies.
 // attn_decode_bf16: one query per sequence; one workgroup per (sequence,
-//   head) streams the whole cache with whole-row loads and merges its four
-//   waves' partial softmax results in LDS.  attn_decode_split (+ combine):
-//   the fp32 path, 64-key chunks merged by a second kernel in chunk order.
+//   head, chunk of keys) with whole-row loads, chunks merged in chunk order
+//   by the last workgroup of a (sequence, head).  attn_decode_split (+
+//   combine): the fp32 path, 64-key chunks merged by a second kernel in
+//   chunk order.
 #include <math.h>
 
 #include <type_traits>
@@ -486,14 +487,24 @@ __global__ __launch_bounds__(256) void attn_decode_split_kernel(AttnDecodeArgs a
     if (tid == 0) { part[HD] = sml[0]; part[HD + 1] = sml[1]; }
 }
 
-// bf16 decode attention, one workgroup per (sequence, query head) over the
-// whole cache.  The four waves take consecutive quarters of the keys; a wave
-// loads 8 K rows and the matching 8 V rows per round in one burst (a load
-// instruction covers whole 128-byte row segments: 8 keys of 64 dims or 4
-// keys of 128) with non-temporal loads, keeps a running max / sum / weighted
-// V per lane, and the waves' results are merged through LDS in wave order.
-// The key split depends only on the sequence length, so a sequence's output
-// does not depend on the rest of the batch.
+// bf16 decode attention.  A sequence of kv_len keys is cut into
+// nch = ceil(kv_len / attn_decode_chunk(HD)) chunks of equal length (the last
+// shorter), a function of its length only; one workgroup per (sequence,
+// query head, chunk).  Its four waves take consecutive quarters of the chunk;
+// a wave loads 8 K rows and the matching 8 V rows per lane per round in one
+// burst (a load instruction covers whole 128-byte row segments: 8 keys of 64
+// dims or 4 keys of 128) with non-temporal loads, keeps a running max / sum /
+// weighted V, and the waves' states merge through LDS in wave order.  A
+// one-chunk sequence writes its output there; with more chunks every
+// workgroup stores its chunk state, and the workgroup that finishes a
+// (sequence, head) last (a device-scope counter, left at zero again) merges
+// the chunks in chunk order.  A sequence's bits therefore depend on its
+// length only -- not on the batch, the grid or the order in which workgroups
+// finish.  Chunks are long (512 keys at head dim 128): measured on the
+// 7B-class decode, 128-key chunks (three to twelve times the workgroups, one
+// load round each) streamed the cache 16 % slower than whole-sequence
+// workgroups, the per-workgroup latency chain (block table, K/V, merge)
+// outweighing the added parallelism; the split serves long sequences.
 
 // 16-byte load marked non-temporal: each K/V row is read once per decode
 // step, and streaming loads keep it from displacing cached data (measured:
@@ -504,6 +515,8 @@ EBRL_DEV uint4 ld_stream16(const bf16_t* p) {
     return make_uint4(v.x, v.y, v.z, v.w);
 }
 
+template <int HD> constexpr int attn_decode_chunk() { return 65536 / HD; }
+
 template <int HD>
 __global__ __launch_bounds__(256) void attn_decode_bf16_kernel(AttnDecodeArgs a, float scale_log2)
 {
@@ -511,26 +524,34 @@ __global__ __launch_bounds__(256) void attn_decode_bf16_kernel(AttnDecodeArgs a,
     constexpr int KPL = 64 / LPK;      // keys per wave load
     constexpr int NL = 8;              // K (and V) loads per lane per round
     constexpr int KW = KPL * NL;       // keys per round
-    __shared__ int s_bt[ATTN_BT_MAX];
+    constexpr int CK = attn_decode_chunk<HD>();
+    constexpr int CB = CK / KV_BLOCK;  // cache blocks per chunk
+    __shared__ int s_bt[CB + 1];       // a chunk may start inside a block
     __shared__ float s_o[4][HD];
     __shared__ float s_ml[4][2];
+    __shared__ int s_last;
 
-    const int i = blockIdx.x, h = blockIdx.y;
+    const int i = blockIdx.x, h = blockIdx.y, c = blockIdx.z;
     const int kvlen = a.kv_len[i];
+    const int nch = max(1, (kvlen + CK - 1) / CK);
+    if (c >= nch) return;              // the grid covers the longest sequence
+    const int clen = (kvlen + nch - 1) / nch;
+    const int c0 = min(kvlen, c * clen), c1 = min(kvlen, c0 + clen);
     const int env = a.seq_env[i];
     const int hkv = a.kv.kv_heads;
     const int kvh = h / (a.q_heads / hkv);
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int sub = lane % LPK, kq = lane / LPK;
-    const int nblk = (kvlen + KV_BLOCK - 1) / KV_BLOCK;
-    for (int b = tid; b < nblk; b += 256) s_bt[b] = a.kv.block_table[(size_t)env * a.kv.bt_stride + b];
+    const int b0 = c0 >> 4;
+    for (int b = tid; b < ((c1 + KV_BLOCK - 1) >> 4) - b0; b += 256)
+        s_bt[b] = a.kv.block_table[(size_t)env * a.kv.bt_stride + b0 + b];
     float q[8];
     load8<bf16_t>((const bf16_t*)a.Q + (size_t)i * a.ldq + h * HD + sub * 8, q);
     __syncthreads();
 
-    const int per = (kvlen + 3) / 4;
-    const int wb = min(kvlen, wave * per), we = min(kvlen, wb + per);
+    const int per = (c1 - c0 + 3) / 4;
+    const int wb = min(c1, c0 + wave * per), we = min(c1, wb + per);
     const size_t blk_elems = (size_t)2 * hkv * KV_BLOCK * HD;
     const bf16_t* kbase = (const bf16_t*)a.kv.base + (size_t)kvh * KV_BLOCK * HD + sub * 8;
     const bf16_t* vbase = kbase + (size_t)hkv * KV_BLOCK * HD;
@@ -543,7 +564,7 @@ __global__ __launch_bounds__(256) void attn_decode_bf16_kernel(AttnDecodeArgs a,
 #pragma unroll
         for (int t = 0; t < NL; ++t) {
             const int key = min(kb + t * KPL + kq, we - 1);
-            const size_t off = (size_t)s_bt[key >> 4] * blk_elems + (size_t)(key & 15) * HD;
+            const size_t off = (size_t)s_bt[(key >> 4) - b0] * blk_elems + (size_t)(key & 15) * HD;
             kr[t] = ld_stream16(kbase + off);
             vr[t] = ld_stream16(vbase + off);
         }
@@ -592,19 +613,51 @@ __global__ __launch_bounds__(256) void attn_decode_bf16_kernel(AttnDecodeArgs a,
     }
     if (lane == 0) { s_ml[wave][0] = m_run; s_ml[wave][1] = l_run; }
     __syncthreads();
+    // the chunk's state: the four waves merged in wave order
+    float M = -INFINITY, L = 0.f, o = 0.f;
     if (tid < HD) {
-        float M = -INFINITY;
 #pragma unroll
         for (int w = 0; w < 4; ++w) M = fmaxf(M, s_ml[w][0]);
-        float L = 0.f, o = 0.f;
 #pragma unroll
         for (int w = 0; w < 4; ++w) {
             const float wt = (s_ml[w][0] == -INFINITY) ? 0.f : fast_exp2(s_ml[w][0] - M);
             L += wt * s_ml[w][1];
             o += wt * s_o[w][tid];
         }
-        st_elem<bf16_t>((bf16_t*)a.O + (size_t)i * a.ldo + h * HD + tid, kvlen > 0 ? o / L : 0.f);
     }
+    bf16_t* const out = (bf16_t*)a.O + (size_t)i * a.ldo + h * HD;
+    if (nch == 1) {
+        if (tid < HD) st_elem<bf16_t>(out + tid, kvlen > 0 ? o / L : 0.f);
+        return;
+    }
+    // several chunks: store this chunk's state, the last workgroup merges
+    const int sh = i * a.q_heads + h;
+    const __amdgpu_buffer_rsrc_t part = coherent_rsrc(a.part + (size_t)sh * a.max_splits * (HD + 2));
+    if (tid < HD) st_coherent1(part, (c * (HD + 2) + tid) * 4, o);
+    if (tid == 0) {
+        st_coherent1(part, (c * (HD + 2) + HD) * 4, M);
+        st_coherent1(part, (c * (HD + 2) + HD + 1) * 4, L);
+    }
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+    if (tid == 0)
+        s_last = __hip_atomic_fetch_add(a.counters + sh, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
+                 (unsigned)(nch - 1);
+    __syncthreads();
+    if (!s_last) return;
+    if (tid < HD) {
+        float Mt = -INFINITY;
+        for (int k = 0; k < nch; ++k) Mt = fmaxf(Mt, ld_coherent1(part, (k * (HD + 2) + HD) * 4));
+        float Lt = 0.f, ot = 0.f;
+        for (int k = 0; k < nch; ++k) {
+            const float mk = ld_coherent1(part, (k * (HD + 2) + HD) * 4);
+            const float wt = (mk == -INFINITY) ? 0.f : fast_exp2(mk - Mt);
+            Lt += wt * ld_coherent1(part, (k * (HD + 2) + HD + 1) * 4);
+            ot += wt * ld_coherent1(part, (k * (HD + 2) + tid) * 4);
+        }
+        st_elem<bf16_t>(out + tid, ot / Lt);
+    }
+    if (tid == 0) __hip_atomic_store(a.counters + sh, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 // grid (n, q_heads), HD threads
@@ -630,18 +683,17 @@ void attn_decode(const AttnDecodeArgs& a, hipStream_t s) {
     const int hd = a.kv.head_dim;
     const float scale_log2 = 1.4426950408889634f / sqrtf((float)hd);
     dim3 g1(a.n, a.q_heads, a.max_splits), g2(a.n, a.q_heads);
-    if (a.bf16 && a.kv.bt_stride <= ATTN_BT_MAX) {
-        if (hd == 64)
-            hipLaunchKernelGGL(attn_decode_bf16_kernel<64>, g2, dim3(256), 0, s, a, scale_log2);
-        else
-            hipLaunchKernelGGL(attn_decode_bf16_kernel<128>, g2, dim3(256), 0, s, a, scale_log2);
-    } else if (a.bf16) {
+    if (a.bf16) {
+        // chunks of the longest sequence the part buffer is laid out for
+        const int keys = a.max_splits * ATTN_DEC_CHUNK;
         if (hd == 64) {
-            hipLaunchKernelGGL((attn_decode_split_kernel<bf16_t, 64>), g1, dim3(256), 0, s, a, scale_log2);
-            hipLaunchKernelGGL((attn_decode_combine_kernel<bf16_t, 64>), g2, dim3(64), 0, s, a);
+            constexpr int CK = attn_decode_chunk<64>();
+            hipLaunchKernelGGL(attn_decode_bf16_kernel<64>, dim3(a.n, a.q_heads, (keys + CK - 1) / CK), dim3(256), 0,
+                               s, a, scale_log2);
         } else {
-            hipLaunchKernelGGL((attn_decode_split_kernel<bf16_t, 128>), g1, dim3(256), 0, s, a, scale_log2);
-            hipLaunchKernelGGL((attn_decode_combine_kernel<bf16_t, 128>), g2, dim3(128), 0, s, a);
+            constexpr int CK = attn_decode_chunk<128>();
+            hipLaunchKernelGGL(attn_decode_bf16_kernel<128>, dim3(a.n, a.q_heads, (keys + CK - 1) / CK), dim3(256), 0,
+                               s, a, scale_log2);
         }
     } else {
         if (hd == 64) {

@@ -117,6 +117,7 @@ struct ebrl_policy {
     float* dec_mar = nullptr;
     float* part = nullptr;     // decode attention partials
     size_t part_floats = 0;
+    unsigned* attn_counters = nullptr;  // decode attention chunk counters [dec_cap][q_heads] (zero between calls)
     float* flow_x = nullptr;
     float* flow_v0 = nullptr;
     float* flow_f = nullptr;   // frame latents being denoised
@@ -521,7 +522,7 @@ int run_block(ebrl_policy* p, BlockCall& b) {
     run_gemm(p, g, b.decode);
     if (b.decode) {
         b.dec.bf16 = p->bf16; b.dec.Q = p->Qb; b.dec.ldq = qn; b.dec.O = p->Ob; b.dec.ldo = qn;
-        b.dec.q_heads = s.hq; b.dec.kv = b.kv; b.dec.part = p->part;
+        b.dec.q_heads = s.hq; b.dec.kv = b.kv; b.dec.part = p->part; b.dec.counters = p->attn_counters;
         prof_begin(p, EBRL_K_ATTN_DECODE);
         attn_decode(b.dec, p->stream);
         prof_end(p, b.attn_flop, b.attn_bytes);
@@ -990,6 +991,11 @@ int ebrl_policy_create(const ebrl_config* config, uint64_t seed, ebrl_policy** o
     const int max_splits = (c.max_seq + p->tail + ATTN_DEC_CHUNK - 1) / ATTN_DEC_CHUNK;
     p->part_floats = (size_t)std::max(c.max_envs, p->dec_cap) * c.q_heads * max_splits * (c.head_dim + 2);
     if ((rc = dev_alloc_t(p, &p->part, p->part_floats))) return bail(rc);
+    {
+        const size_t words = (size_t)std::max(c.max_envs, p->dec_cap) * c.q_heads;
+        if ((rc = dev_alloc_t(p, &p->attn_counters, words))) return bail(rc);
+        HIPCHK(p, hipMemset(p->attn_counters, 0, words * 4));
+    }
     if (c.exp_layers) {
         const size_t act_rows = (size_t)c.max_envs * c.chunk;
         if ((rc = dev_alloc_t(p, &p->flow_x, act_rows * c.adim))) return bail(rc);

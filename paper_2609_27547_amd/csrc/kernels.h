@@ -91,8 +91,9 @@ void attn_prefill(const AttnPrefillArgs& a, hipStream_t s);
 // many 16-token blocks (4096 tokens) per sequence.
 constexpr int ATTN_BT_MAX = 256;
 
-// One query per sequence against kv_len[i] keys, split over the sequence
-// in chunks of ATTN_DEC_CHUNK keys, then combined in chunk order.
+// One query per sequence against kv_len[i] keys, split over the sequence in
+// chunks (fp32: ATTN_DEC_CHUNK keys; bf16: at most 512 keys at head dim 128,
+// 1024 at 64) merged in chunk order.
 constexpr int ATTN_DEC_CHUNK = 64;
 struct AttnDecodeArgs {
     bool bf16 = true;
@@ -103,8 +104,10 @@ struct AttnDecodeArgs {
     const int* seq_env = nullptr;
     const int* kv_len = nullptr;
     int n = 0;
-    int max_splits = 0;            // ceil(max kv_len / chunk) over the call
+    int max_splits = 0;            // ceil(longest kv_len / ATTN_DEC_CHUNK) the buffers are sized for
     float* part = nullptr;         // [n][q_heads][max_splits][hd + 2]
+    // bf16: [n][q_heads] zeroed words (left zero after the call)
+    unsigned* counters = nullptr;
 };
 void attn_decode(const AttnDecodeArgs& a, hipStream_t s);
 

@@ -610,6 +610,36 @@ def test_bf16_attention_at_block_and_tile_boundaries(hd):
     pol.close()
 
 
+@pytest.mark.parametrize("hd", [64, 128])
+def test_bf16_decode_attention_splits_long_sequences(hd):
+    """Decode attention cuts a sequence into chunks (at most 512 keys at head
+    dim 128, 1024 at 64) by its length alone and merges them in chunk order:
+    prefixes on both sides of one, two and three chunks against the oracle,
+    and each env's tokens and margins bitwise equal whether it is decoded
+    alone or in the batch."""
+    ck = 65536 // hd
+    lens = [ck - 6, ck - 5, ck + 1, 2 * ck + 7, 3 * ck - 9, 17]
+    o = dataclasses.replace(TINY_LANG, head_dim=hd, q_heads=4 if hd == 64 else 2, kv_heads=2 if hd == 64 else 1,
+                            n_lang=max(lens))
+    ids = list(range(len(lens)))
+    _, lang = _obs(o, ids, 1009)
+    pol = E.Policy(_ebrl_config(o, len(ids), max(lens)), seed=0)
+    pol.prefill(ids, images=None, lang_ids=_dev(lang), lang_len=lens)
+    tok, _, mar = pol.decode_actions(ids)
+    torch.cuda.synchronize()
+    ref = M.Policy(o, seed=0)
+    for e, T in zip(ids, lens):
+        st = ref.prefill(None, lang[e][:T])
+        assert P.row_rel_err(pol.read_state(E.STATE_H_LAST_PRE, e), st.h_last_pre) < P.TOL_BF16
+        r = ref.decode(st, forced=tok[e, :-1].cpu().numpy())
+        P.check_tokens(tok[e].cpu().numpy(), r)
+        _check_margins(pol, ref, e, mar[e].cpu().numpy(), r, P.TOL_BF16)
+        t1, _, m1 = pol.decode_actions([e])
+        torch.cuda.synchronize()
+        assert torch.equal(t1[0], tok[e]) and torch.equal(m1[0], mar[e])
+    pol.close()
+
+
 def test_stream_read_reference_kernel():
     # the HBM read reference: argument checks, and a run that reads every
     # byte without writing its output (the fold of 1-filled words is not the
