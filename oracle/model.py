@@ -374,20 +374,32 @@ class DecodeResult:
     actions: np.ndarray          # [7]
 
 
+# Where a bf16 policy stores activations in bf16 (diagnostic emulation):
+# normalised rows and patches entering a GEMM, rotated Q, the K/V cache,
+# softmax numerators before the P.V product, attention and SwiGLU outputs.
+BF16_POINTS = ("gemm_in", "q", "kv", "p", "attn_out", "swiglu_out")
+
+
 class Policy:
     """Seeded random-init policy evaluated in float64."""
 
     def __init__(self, cfg: Config, seed: int = 0, overrides: Optional[Dict[str, np.ndarray]] = None,
-                 cache_limit_params: int = 600_000_000, emulate_bf16: bool = False):
+                 cache_limit_params: int = 600_000_000, emulate_bf16=False):
         self.cfg = cfg
         self.seed = seed
         # Optional diagnostic: round to bf16 where a bf16 policy stores
-        # activations in bf16 (normalised GEMM inputs, rotated Q and K, V,
-        # softmax numerators before the P.V product, attention and SwiGLU
-        # outputs, patch pixels); all arithmetic between those points stays
-        # float64.  Off by default; parity is always judged against the exact
-        # mode, never against this one.
-        self.emulate_bf16 = bool(emulate_bf16 and cfg.bf16)
+        # activations in bf16; all arithmetic between those points stays
+        # float64.  emulate_bf16 is True (every point) or a collection of
+        # point names from BF16_POINTS.  Off by default; parity is always
+        # judged against the exact mode, never against this one.
+        if emulate_bf16 is True:
+            points = set(BF16_POINTS)
+        else:
+            points = set(emulate_bf16 or ())
+            if not points <= set(BF16_POINTS):
+                raise ValueError(f"unknown bf16 storage points {points - set(BF16_POINTS)}")
+        self.bf16_points = points if cfg.bf16 else set()
+        self.emulate_bf16 = bool(self.bf16_points)
         self.shapes = tensor_shapes(cfg)
         self.overrides = dict(overrides or {})
         total = sum(int(np.prod(sh)) for _, sh in self.shapes.values())
@@ -420,7 +432,7 @@ class Policy:
     def _prenorm(self, x):
         """Operand of the projection after a pre-norm: the normalised row
         (rounded to bf16 when emulating bf16 storage)."""
-        return self._r(rmsnorm(x, self.cfg.eps))
+        return self._r(rmsnorm(x, self.cfg.eps), "gemm_in")
 
     def block(self, x, Wl, n_heads, n_kv, hd, pos, past_k=None, past_v=None, past_pos=None,
               causal=True, use_rope=True):
@@ -434,25 +446,25 @@ class Policy:
         if use_rope:
             q = rope(q, pos, self.cfg.rope_base)
             k = rope(k, pos, self.cfg.rope_base)
-        q, k, v = R(q), R(k), R(v)
+        q, k, v = R(q, "q"), R(k, "kv"), R(v, "kv")
         if past_k is not None:
             K = np.concatenate([past_k, k], axis=0)
             V = np.concatenate([past_v, v], axis=0)
             kpos = np.concatenate([past_pos, pos])
         else:
             K, V, kpos = k, v, pos
-        if self.emulate_bf16:
+        if "p" in self.bf16_points:
             o = self._attention_bf16(q, K, V, pos, kpos, causal)
         else:
             o = multihead_attention(q, K, V, pos, kpos, causal)
-        o = R(o.reshape(t, n_heads * hd))
+        o = R(o.reshape(t, n_heads * hd), "attn_out")
         x = x + linear(o, Wl["o"])
         h = self._prenorm(x)
-        x = x + linear(R(silu(linear(h, Wl["gate"])) * linear(h, Wl["up"])), Wl["down"])
+        x = x + linear(R(silu(linear(h, Wl["gate"])) * linear(h, Wl["up"]), "swiglu_out"), Wl["down"])
         return x, k, v
 
-    def _r(self, a):
-        return f64_to_bf16_value(a) if self.emulate_bf16 else a
+    def _r(self, a, point):
+        return f64_to_bf16_value(a) if point in self.bf16_points else a
 
     @staticmethod
     def _attention_bf16(q, k, v, q_pos, k_pos, causal):
@@ -476,7 +488,7 @@ class Policy:
         cfg = self.cfg
         rows = []
         if image is not None:
-            patches = self._r(patchify(np.asarray(image, dtype=np.float64), cfg.patch))
+            patches = self._r(patchify(np.asarray(image, dtype=np.float64), cfg.patch), "gemm_in")
             if cfg.vit_layers:
                 v = linear(patches, self.W("W_pe")) + self.W("vit_pos")
                 hd = cfg.vit_d // cfg.vit_heads
@@ -484,7 +496,7 @@ class Policy:
                 for l in range(cfg.vit_layers):
                     v, _, _ = self.block(v, self.layer("vit", l), cfg.vit_heads, cfg.vit_heads, hd,
                                          pos, causal=False, use_rope=False)
-                rows.append(linear(self._r(rmsnorm(v, cfg.eps)), self.W("W_proj")))
+                rows.append(linear(self._r(rmsnorm(v, cfg.eps), "gemm_in"), self.W("W_proj")))
             else:
                 rows.append(linear(patches, self.W("W_pe")))
         E = self.W("E_lang")

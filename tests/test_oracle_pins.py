@@ -655,6 +655,16 @@ def test_bf16_emulation_rounds_only_at_storage_points():
     # equal scores: every numerator is exactly 1 -> the mean of V
     same = M.Policy._attention_bf16(np.zeros((3, 1, 16)), k[:4], v[:4], np.arange(3) + 9, kp[:4], True)
     assert np.allclose(same, np.repeat(v[:4].mean(0, keepdims=True), 3, axis=0), atol=1e-15)
+    # storage points one at a time: with only the cache rounded, layer 0's
+    # K and V are the exact ones rounded (its inputs are exact) and Q-only
+    # rounding leaves layer 0's K/V untouched
+    kv_only = M.Policy(cfg16, seed=0, emulate_bf16={"kv"}).prefill(img[0], lang[0])
+    q_only = M.Policy(cfg16, seed=0, emulate_bf16={"q"}).prefill(img[0], lang[0])
+    assert np.array_equal(kv_only.k[0], M.f64_to_bf16_value(a.k[0]))
+    assert np.array_equal(kv_only.v[0], M.f64_to_bf16_value(a.v[0]))
+    assert np.array_equal(q_only.k[0], a.k[0]) and not np.array_equal(q_only.k[1], a.k[1])
+    with pytest.raises(ValueError):
+        M.Policy(cfg16, seed=0, emulate_bf16={"weights"})
     # a whole emulated decode stays within rounding of the exact one
     ex = M.Policy(cfg16, seed=0)
     ra = ex.decode(a)
