@@ -560,21 +560,32 @@ def main():
         phase["head"] += pe[1].elapsed_time(pe[2]) / reps
     pol.profile_enable([])
     kernels = {}
+    class_work = {}
     for cls, name in E.KERNEL_CLASSES.items():
         r = pol.profile_read(cls, reset=True)
+        class_work[cls] = r
         if r["launches"]:
             kernels[name] = {"launches_per_step": r["launches"] / reps, "ms_per_step": round(r["ms"] / reps, 4),
                              "tflops": round(r["flop"] / (r["ms"] * 1e9), 1) if r["ms"] else None,
                              "gbs": round(r["bytes"] / (r["ms"] * 1e6), 1) if r["ms"] else None}
 
-    # roofline fraction of every kernel class (breakdown pass, per-launch events)
+    # roofline fraction of every kernel class (breakdown pass, per-launch
+    # events): the class's algorithmic flops and bytes give the time it
+    # cannot beat, max(flop / peak flop rate, bytes / peak HBM rate); the
+    # larger term names the bound, and frac is that time over the measured
+    # one (prefill attention over a few hundred keys has an arithmetic
+    # intensity well below the chip's balance point, so HBM bounds it)
     fractions = {}
-    for name, k in kernels.items():
-        if name in ("gemm", "attn_prefill") and k["tflops"] is not None:
-            fractions[name] = {"bound": "mfma", "achieved_tflops": k["tflops"],
-                               "frac": round(k["tflops"] / (PEAK_BF16_TFLOPS if pol.bf16 else PEAK_FP32_TFLOPS), 4)}
-        elif name in ("gemm_skinny", "attn_decode") and k["gbs"] is not None:
-            fractions[name] = {"bound": "hbm", "achieved_gbs": k["gbs"], "frac": round(k["gbs"] / PEAK_HBM_GBS, 4)}
+    peak_flops = (PEAK_BF16_TFLOPS if pol.bf16 else PEAK_FP32_TFLOPS) * 1e12
+    for cls, name in E.KERNEL_CLASSES.items():
+        k, r = kernels.get(name), class_work[cls]
+        if k is None or not r["ms"] or name == "other":
+            continue
+        t_flop, t_byte = r["flop"] / peak_flops, r["bytes"] / (PEAK_HBM_GBS * 1e9)
+        t = r["ms"] / 1e3
+        fractions[name] = {"bound": "mfma" if t_flop >= t_byte else "hbm", "achieved_tflops": k["tflops"],
+                           "achieved_gbs": k["gbs"], "flop_per_byte": round(r["flop"] / r["bytes"], 1) if r["bytes"] else None,
+                           "frac": round(max(t_flop, t_byte) / t, 4)}
 
     # ---- optional: the same steps on CU-masked partitions (the stand-in for SM quotas)
     partitions = None

@@ -61,6 +61,111 @@ EBRL_DEV float attn_sum_xor16_32(float v) {
     return __builtin_bit_cast(float, (unsigned)b[0]) + __builtin_bit_cast(float, (unsigned)b[1]);
 }
 
+// One 64-key tile of the online-softmax attention for the wave's 16
+// queries (lane (r, g): query r, keys 16 kt + 4 g + v): scores S^T = K Q^T on
+// MFMA, masking, the integer running maximum, P, and O^T += V^T P^T.  tk / tv
+// point at the tile's K and V rows in LDS (64 rows of HD, 16-byte chunks
+// swizzled by row).
+template <int HD>
+EBRL_DEV void attn_tile_math(const bf16_t* tk, const bf16_t* tv, int k0, int mask_from, int key_lim,
+                             float scale_log2, const bf16x8 (&qb)[HD / 32], float& m_i, float& l_i,
+                             f32x4 (&acc)[HD / 16], int lane)
+{
+    constexpr int KT = 64, CPR = HD / 8;
+    const int r = lane & 15, g = lane >> 4;
+    // S^T tiles: lane holds key 16kt + 4g + v for query r
+    f32x4 s[4];
+#pragma unroll
+    for (int kt = 0; kt < 4; ++kt) {
+        s[kt] = f32x4{0.f, 0.f, 0.f, 0.f};
+        const int row = kt * 16 + r;
+#pragma unroll
+        for (int ks = 0; ks < HD / 32; ++ks) {
+            const bf16x8 ka =
+                *reinterpret_cast<const bf16x8*>(tk + (row * CPR + ((ks * 4 + g) ^ (row & (CPR - 1)))) * 8);
+            s[kt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka, qb[ks], s[kt], 0, 0, 0);
+        }
+    }
+    // Row maximum of the raw scores: the scale is positive, so it
+    // commutes with the maximum and is applied once, inside the
+    // exponent's fused multiply-add.  Masked scores become -inf.
+    if (mask_from <= k0 + KT - 1) {
+        // tile reaches past the keys or past a query of this wave: key
+        // k0 + 16 kt + 4 g + v is visible to this lane's query iff
+        // 16 kt + v < lim
+        const int lim = key_lim - k0 - 4 * g;
+#pragma unroll
+        for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) s[kt][v] = kt * 16 + v < lim ? s[kt][v] : -INFINITY;
+    }
+    float tmax = -INFINITY;
+#pragma unroll
+    for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) tmax = fmaxf(tmax, s[kt][v]);
+    tmax = attn_max_xor16_32(tmax);
+    // The running maximum is kept as an integer (ceil, in log2 units):
+    // rescaling by alpha is then a power of two, which commutes with the
+    // bf16 rounding of P, so P is rounded as 2^(x - ceil(row max)) no
+    // matter how the keys are split into tiles.
+    const float m_new = fmaxf(m_i, ceilf(tmax * scale_log2));
+    const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
+    const float alpha = (m_i == -INFINITY) ? 0.f : ldexpf(1.0f, (int)(m_i - m_use));
+    float psum = 0.f;
+#pragma unroll
+    for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+            const float p = fast_exp2(fmaf(s[kt][v], scale_log2, -m_use));
+            s[kt][v] = p;
+            psum += p;
+        }
+    psum = attn_sum_xor16_32(psum);
+    l_i = l_i * alpha + psum;
+    m_i = m_new;
+    // alpha is a power of two (1 once the integer running maximum stops
+    // growing), so the rescale is exact; it is applied unconditionally, which
+    // keeps the accumulators in place (a branch around it costs register
+    // copies on both paths)
+#pragma unroll
+    for (int i = 0; i < HD / 16; ++i) acc[i] *= alpha;
+
+    // O^T += V^T P^T.  V stays row-major in LDS; ds_read_b64_tr_b16 hands
+    // lane (r, g) the values of dimension 16 dt + r for 4 keys per read
+    // (keys 32 ks2 + 4g + j, then 32 ks2 + 16 + 4g + j), the same key
+    // order the score lanes hold.
+    const int a16 = lane & 15;
+#pragma unroll
+    for (int ks2 = 0; ks2 < 2; ++ks2) {
+        bf16x8 pb;
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+            pb[v] = (__bf16)s[2 * ks2][v];
+            pb[4 + v] = (__bf16)s[2 * ks2 + 1][v];
+        }
+#pragma unroll
+        for (int dt = 0; dt < HD / 16; ++dt) {
+            const int d = dt * 16 + 4 * (a16 & 3);
+            attn_v4s lo, hi;
+            {
+                const int key = 32 * ks2 + 4 * g + (a16 >> 2);
+                const int off = (key * CPR + ((d >> 3) ^ (key & (CPR - 1)))) * 8 + (d & 7);
+                lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) attn_v4s*)(attn_lds_ptr_t)(tv + off));
+            }
+            {
+                const int key = 32 * ks2 + 16 + 4 * g + (a16 >> 2);
+                const int off = (key * CPR + ((d >> 3) ^ (key & (CPR - 1)))) * 8 + (d & 7);
+                hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) attn_v4s*)(attn_lds_ptr_t)(tv + off));
+            }
+            const uint2 lo2 = __builtin_bit_cast(uint2, lo), hi2 = __builtin_bit_cast(uint2, hi);
+            const uint4 w = make_uint4(lo2.x, lo2.y, hi2.x, hi2.y);
+            const bf16x8 va = __builtin_bit_cast(bf16x8, w);
+            acc[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, pb, acc[dt], 0, 0, 0);
+        }
+    }
+}
+
 // One workgroup per (query tile of ATTN_Q_TILE rows, head): NW waves of 16
 // queries share every K/V tile staged in LDS, which each wave then skips if
 // none of its queries can see it.
@@ -198,103 +303,7 @@ __global__ __launch_bounds__(64 * NW) void attn_prefill_bf16_kernel(AttnPrefillA
         // (processing it would leave m, l and acc as they are)
         if (k0 >= wave_keys) return;
 
-        // S^T tiles: lane holds key 16kt + 4g + v for query r
-        f32x4 s[4];
-#pragma unroll
-        for (int kt = 0; kt < 4; ++kt) {
-            s[kt] = f32x4{0.f, 0.f, 0.f, 0.f};
-            const int row = kt * 16 + r;
-#pragma unroll
-            for (int ks = 0; ks < HD / 32; ++ks) {
-                const bf16x8 ka =
-                    *reinterpret_cast<const bf16x8*>(tk + (row * CPR + ((ks * 4 + g) ^ (row & (CPR - 1)))) * 8);
-                s[kt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka, qb[ks], s[kt], 0, 0, 0);
-            }
-        }
-        // Row maximum of the raw scores: the scale is positive, so it
-        // commutes with the maximum and is applied once, inside the
-        // exponent's fused multiply-add.  Masked scores become -inf.
-        float tmax = -INFINITY;
-        if (mask_from <= k0 + KT - 1) {
-            // tile reaches past the keys or past a query of this wave: key
-            // k0 + 16 kt + 4 g + v is visible to this lane's query iff
-            // 16 kt + v < lim
-            const int lim = key_lim - k0 - 4 * g;
-#pragma unroll
-            for (int kt = 0; kt < 4; ++kt)
-#pragma unroll
-                for (int v = 0; v < 4; ++v) {
-                    const float val = kt * 16 + v < lim ? s[kt][v] : -INFINITY;
-                    s[kt][v] = val;
-                    tmax = fmaxf(tmax, val);
-                }
-        } else {
-#pragma unroll
-            for (int kt = 0; kt < 4; ++kt)
-#pragma unroll
-                for (int v = 0; v < 4; ++v) tmax = fmaxf(tmax, s[kt][v]);
-        }
-        tmax = attn_max_xor16_32(tmax);
-        // The running maximum is kept as an integer (ceil, in log2 units):
-        // rescaling by alpha is then a power of two, which commutes with the
-        // bf16 rounding of P, so P is rounded as 2^(x - ceil(row max)) no
-        // matter how the keys are split into tiles.
-        const float m_new = fmaxf(m_i, ceilf(tmax * scale_log2));
-        const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
-        const float alpha = (m_i == -INFINITY) ? 0.f : ldexpf(1.0f, (int)(m_i - m_use));
-        float psum = 0.f;
-#pragma unroll
-        for (int kt = 0; kt < 4; ++kt)
-#pragma unroll
-            for (int v = 0; v < 4; ++v) {
-                const float p = fast_exp2(fmaf(s[kt][v], scale_log2, -m_use));
-                s[kt][v] = p;
-                psum += p;
-            }
-        psum = attn_sum_xor16_32(psum);
-        l_i = l_i * alpha + psum;
-        m_i = m_new;
-        // alpha is a power of two that is 1 once the integer running maximum
-        // stops growing: skip the rescale (exact either way) when it is 1 in
-        // every lane
-        if (__any(alpha != 1.0f)) {
-#pragma unroll
-            for (int i = 0; i < HD / 16; ++i) acc[i] *= alpha;
-        }
-
-        // O^T += V^T P^T.  V stays row-major in LDS; ds_read_b64_tr_b16 hands
-        // lane (r, g) the values of dimension 16 dt + r for 4 keys per read
-        // (keys 32 ks2 + 4g + j, then 32 ks2 + 16 + 4g + j), the same key
-        // order the score lanes hold.
-        const int a16 = lane & 15;
-#pragma unroll
-        for (int ks2 = 0; ks2 < 2; ++ks2) {
-            bf16x8 pb;
-#pragma unroll
-            for (int v = 0; v < 4; ++v) {
-                pb[v] = (__bf16)s[2 * ks2][v];
-                pb[4 + v] = (__bf16)s[2 * ks2 + 1][v];
-            }
-#pragma unroll
-            for (int dt = 0; dt < HD / 16; ++dt) {
-                const int d = dt * 16 + 4 * (a16 & 3);
-                attn_v4s lo, hi;
-                {
-                    const int key = 32 * ks2 + 4 * g + (a16 >> 2);
-                    const int off = (key * CPR + ((d >> 3) ^ (key & (CPR - 1)))) * 8 + (d & 7);
-                    lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) attn_v4s*)(attn_lds_ptr_t)(tv + off));
-                }
-                {
-                    const int key = 32 * ks2 + 16 + 4 * g + (a16 >> 2);
-                    const int off = (key * CPR + ((d >> 3) ^ (key & (CPR - 1)))) * 8 + (d & 7);
-                    hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) attn_v4s*)(attn_lds_ptr_t)(tv + off));
-                }
-                const uint2 lo2 = __builtin_bit_cast(uint2, lo), hi2 = __builtin_bit_cast(uint2, hi);
-                const uint4 w = make_uint4(lo2.x, lo2.y, hi2.x, hi2.y);
-                const bf16x8 va = __builtin_bit_cast(bf16x8, w);
-                acc[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, pb, acc[dt], 0, 0, 0);
-            }
-        }
+        attn_tile_math<HD>(tk, tv, k0, mask_from, key_lim, scale_log2, qb, m_i, l_i, acc, lane);
     };
 
     if (ntiles > 0) dma(0, 0);

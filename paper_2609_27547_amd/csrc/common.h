@@ -13,12 +13,8 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 
 EBRL_DEV float bf16_to_f32(bf16_t h) { return __uint_as_float(((uint32_t)h) << 16); }
 
-// Round to nearest even (finite inputs).
-EBRL_DEV bf16_t f32_to_bf16(float f) {
-    uint32_t u = __float_as_uint(f);
-    u += 0x7FFFu + ((u >> 16) & 1u);
-    return (bf16_t)(u >> 16);
-}
+// Round to nearest even (v_cvt_pk_bf16_f32).
+EBRL_DEV bf16_t f32_to_bf16(float f) { return __builtin_bit_cast(bf16_t, (__bf16)f); }
 
 // Element loads/stores templated on the storage type (float or bf16_t).
 template <typename T> EBRL_DEV float ld_elem(const T* p);
@@ -34,10 +30,9 @@ template <> EBRL_DEV void st4<float>(float* p, float a, float b, float c, float 
     *reinterpret_cast<float4*>(p) = make_float4(a, b, c, d);
 }
 template <> EBRL_DEV void st4<bf16_t>(bf16_t* p, float a, float b, float c, float d) {
-    uint2 u;
-    u.x = (uint32_t)f32_to_bf16(a) | ((uint32_t)f32_to_bf16(b) << 16);
-    u.y = (uint32_t)f32_to_bf16(c) | ((uint32_t)f32_to_bf16(d) << 16);
-    *reinterpret_cast<uint2*>(p) = u;
+    typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
+    const bf16x4_t v = {(__bf16)a, (__bf16)b, (__bf16)c, (__bf16)d};
+    *reinterpret_cast<bf16x4_t*>(p) = v;
 }
 
 // Cross-lane reductions without LDS round trips where possible: DPP

@@ -691,7 +691,12 @@ int denoise(ebrl_policy* p, const int32_t* env_ids, int32_t n, const float* fnoi
                 b.pre.tile_q0 = md + o_tq0; b.pre.n_tiles = (int)tseq.size(); b.pre.causal = false;
                 b.pre.max_kv_len = c.max_seq + S;   // the graph may serve longer prefixes later
                 b.attn_flop = 0;
-                for (int i = 0; i < n; ++i) b.attn_flop += 4.0 * c.head_dim * p->exp.hq * (double)S * kv_len[i];
+                // algorithmic bytes: Q read and O written once, every K/V row read once
+                b.attn_bytes = 2.0 * n * S * p->exp.hq * c.head_dim * p->esz;
+                for (int i = 0; i < n; ++i) {
+                    b.attn_flop += 4.0 * c.head_dim * p->exp.hq * (double)S * kv_len[i];
+                    b.attn_bytes += 2.0 * kv_len[i] * p->exp.hkv * c.head_dim * p->esz;
+                }
                 int rc2 = run_block(p, b);
                 if (rc2) return rc2;
             }
@@ -1173,6 +1178,7 @@ int ebrl_prefill(ebrl_policy* p, const ebrl_obs_batch* obs, const int32_t* env_i
                 b.pre.tile_q0 = md + o_vtq0; b.pre.n_tiles = (int)v_tseq.size(); b.pre.causal = false;
                 b.pre.max_kv_len = pv;
                 b.attn_flop = 4.0 * p->vit.hd * p->vit.hq * (double)n * pv * pv;
+                b.attn_bytes = 2.0 * n * pv * (double)(p->vit.hq + p->vit.hkv) * p->vit.hd * p->esz;
                 if ((rc = run_block(p, b))) return rc;
             }
             prof_begin(p, EBRL_K_OTHER);
@@ -1206,7 +1212,8 @@ int ebrl_prefill(ebrl_policy* p, const ebrl_obs_batch* obs, const int32_t* env_i
         b.pre.kv_len = md + o_len; b.pre.tile_seq = md + o_tseq; b.pre.tile_q0 = md + o_tq0;
         b.pre.n_tiles = (int)tiles.size(); b.pre.causal = true; b.pre.max_kv_len = maxT;
         b.attn_flop = 4.0 * c.head_dim * c.q_heads * causal_pairs;
-        b.attn_bytes = 2.0 * kv_rows * c.kv_heads * c.head_dim * p->esz * 2.0;  // Q/O + K/V once
+        // Q read and O written once, every K/V row read once
+        b.attn_bytes = 2.0 * kv_rows * (double)(c.q_heads + c.kv_heads) * c.head_dim * p->esz;
         if ((rc = run_block(p, b))) return rc;
     }
     prof_begin(p, EBRL_K_OTHER);
