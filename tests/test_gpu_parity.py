@@ -102,6 +102,32 @@ def test_decode_gemm_repeat_and_row_subsets_bitwise(N, K):
         assert torch.equal(C, full[:m]), m
 
 
+def test_op_gemm_concurrent_streams_keep_their_own_split_workspace():
+    """ebrl_op_gemm's K-split partial sums and tile counters belong to the
+    (device, stream) pair: two streams running split GEMMs at the same time
+    (4 splits at K = 11008, 8 at 8192) give the bits of the same products run
+    alone, on every one of several interleaved calls."""
+    rng = np.random.default_rng(7)
+    shapes = [(32, 4096, 11008), (48, 2048, 8192)]
+    ops = []
+    for M_, N, K in shapes:
+        A = torch.from_numpy(rng.normal(size=(M_, K)).astype(np.float32)).to(torch.bfloat16).cuda()
+        B = torch.from_numpy(rng.normal(size=(N, K)).astype(np.float32)).to(torch.bfloat16).cuda()
+        ref = torch.empty((M_, N), dtype=torch.float32, device="cuda")
+        E.op_gemm(A, B, ref)
+        ops.append((A, B, ref))
+    torch.cuda.synchronize()
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    outs = [[torch.empty_like(ref) for _ in range(6)] for _, _, ref in ops]
+    for rep in range(6):
+        for i, ((A, B, _), st) in enumerate(zip(ops, streams)):
+            E.op_gemm(A, B, outs[i][rep], stream=st.cuda_stream)
+    torch.cuda.synchronize()
+    for i, (_, _, ref) in enumerate(ops):
+        for rep in range(6):
+            assert torch.equal(outs[i][rep], ref), (i, rep)
+
+
 def test_large_gemm_tile_variants_agree_bitwise():
     """The large-M kernel's macro tile follows the shape: with 4092 columns
     (ragged against both 256 and 128), 9200 rows take 192 x 256 tiles (the
