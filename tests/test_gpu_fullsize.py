@@ -179,8 +179,11 @@ def balanced_mask(frac_quarters: int, n_cu: int = 256):
     return words
 
 
-@pytest.mark.timeout(1200)
-def test_ragged_decode_partitions_bitwise_and_sampled_parity(oracle_7b):
+@pytest.fixture(scope="module")
+def ragged(oracle_7b):
+    """The ragged workload on the GPU (the seeded calls on the whole chip and
+    on a quarter of it, one env alone, the eight sampled envs together) and
+    the exact oracle's teacher-forced pass for each sampled env."""
     cfg = M.PRESETS[3]
     pool = 128
     T = synth_inputs.ragged_prefix_lengths(5, pool, 200, 320)
@@ -193,35 +196,67 @@ def test_ragged_decode_partitions_bitwise_and_sampled_parity(oracle_7b):
         tok, _, mar = pol.decode_actions(ids)
         full.append((tok.clone(), mar.clone()))
     torch.cuda.synchronize()
+    masked = []
     s25 = E.create_cu_masked_stream(0, balanced_mask(1))
     try:
         pol.bind_stream(s25)
-        for ids, (tok_f, mar_f) in zip(calls, full):
+        for ids in calls:
             tok, _, mar = pol.decode_actions(ids)
             torch.cuda.synchronize()
-            assert torch.equal(tok, tok_f) and torch.equal(mar, mar_f)
+            masked.append((tok.clone(), mar.clone()))
         pol.bind_stream(torch.cuda.current_stream().cuda_stream)
     finally:
         torch.cuda.synchronize()
         E.destroy_stream(s25)
-    # the same env decoded alone and inside another batch: bitwise equal
     ids0 = calls[0]
     e = int(ids0[len(ids0) // 2])
-    j = list(ids0).index(e)
     tok_solo, _, mar_solo = pol.decode_actions([e])
     tok_s, _, mar_s = pol.decode_actions(RAGGED_SAMPLE)
     torch.cuda.synchronize()
+    sampled = []
+    for i, env in enumerate(RAGGED_SAMPLE):
+        st, r = oracle_7b.teacher_forced(None, lang[env][:T[env]], tok_s[i, :-1].cpu().numpy())
+        sampled.append((env, st, r))
+    yield dict(pol=pol, calls=calls, full=full, masked=masked, solo=(e, tok_solo, mar_solo),
+               tok_s=tok_s, mar_s=mar_s, sampled=sampled)
+    pol.close()
+
+
+@pytest.mark.timeout(1200)
+def test_ragged_decode_partitions_bitwise_and_sampled_parity(ragged, oracle_7b):
+    """Bitwise: every call's tokens and margins on a quarter of the CUs equal
+    the whole chip's, and an env decoded alone equals the same env inside a
+    call.  Parity of the eight sampled envs at the bounds the oracle's own
+    bf16 storage table gives (RAGGED_TOL, RAGGED_MARGIN)."""
+    pol, calls, full = ragged["pol"], ragged["calls"], ragged["full"]
+    for (tok, mar), (tok_f, mar_f) in zip(ragged["masked"], full):
+        assert torch.equal(tok, tok_f) and torch.equal(mar, mar_f)
+    e, tok_solo, mar_solo = ragged["solo"]
+    j = list(calls[0]).index(e)
     assert torch.equal(tok_solo[0], full[0][0][j]) and torch.equal(mar_solo[0], full[0][1][j])
+    tok_s, mar_s = ragged["tok_s"], ragged["mar_s"]
     if e in RAGGED_SAMPLE:
         assert torch.equal(tok_s[RAGGED_SAMPLE.index(e)], full[0][0][j])
     tok_s, mar_s = tok_s.cpu().numpy(), mar_s.cpu().numpy()
     strict, rows_within_plain = 0, 0
-    for i, e in enumerate(RAGGED_SAMPLE):
-        st, r = oracle_7b.teacher_forced(None, lang[e][:T[e]], tok_s[i, :-1])
-        worst = _check_prefix(pol, e, st, [0, 31], f"ragged{e}", tol=RAGGED_TOL)
+    for i, (env, st, r) in enumerate(ragged["sampled"]):
+        worst = _check_prefix(pol, env, st, [0, 31], f"ragged{env}", tol=RAGGED_TOL)
         rows_within_plain += worst < P.TOL_BF16
-        strict += _check_tokens(tok_s[i], r, f"ragged{e}", thr=RAGGED_MARGIN)
-        _check_margins(pol, oracle_7b, e, mar_s[i], r, f"ragged{e}", tol=RAGGED_TOL)
+        strict += _check_tokens(tok_s[i], r, f"ragged{env}", thr=RAGGED_MARGIN)
+        _check_margins(pol, oracle_7b, env, mar_s[i], r, f"ragged{env}", tol=RAGGED_TOL)
     print(f"RAGGED tokens decided exactly: {strict} of {7 * len(RAGGED_SAMPLE)}; "
           f"envs with every row within 2e-2: {rows_within_plain} of {len(RAGGED_SAMPLE)}", flush=True)
-    pol.close()
+
+
+@pytest.mark.xfail(reason="bf16 storage alone moves these language-only 32-layer prefixes past 2e-2 "
+                          "(python3 -m oracle.bf16_storage_table: 2.5-2.7e-2 from the K/V cache alone, "
+                          "5.1-5.5e-2 from every bf16 storage point)", strict=False)
+def test_ragged_sampled_envs_at_the_plain_bounds(ragged):
+    """The same eight sampled envs held to the plain bounds (2e-2 rows, the
+    1e-2 margin rule): expected to fail for the reason the oracle's storage
+    table gives, kept so that the gap stays visible."""
+    pol = ragged["pol"]
+    tok_s = ragged["tok_s"].cpu().numpy()
+    for i, (env, st, r) in enumerate(ragged["sampled"]):
+        _check_prefix(pol, env, st, [0, 31], f"ragged_plain{env}", tol=P.TOL_BF16)
+        _check_tokens(tok_s[i], r, f"ragged_plain{env}", thr=P.MARGIN)
