@@ -1232,6 +1232,20 @@ int ebrl_decode_actions(ebrl_policy* p, const int32_t* env_ids, int32_t n, int32
     if (n == 0) return EBRL_OK;
     if (!out_tokens) return fail(p, EBRL_E_INVALID, "out_tokens is NULL");
     const int ntok = c.n_action_tokens, steps = ntok - 1;
+    // The decode GEMMs' split plan holds for at most DECODE_MAX_ROWS rows (past
+    // it a different kernel, with another summation order, would take over):
+    // larger calls run as consecutive calls of at most that many envs, so an
+    // env's bits never depend on the call's size.
+    if (n > DECODE_MAX_ROWS) {
+        for (int off = 0; off < n; off += DECODE_MAX_ROWS) {
+            const int m = std::min(DECODE_MAX_ROWS, n - off);
+            const size_t o = (size_t)off * ntok;
+            if ((rc = ebrl_decode_actions(p, env_ids + off, m, out_tokens + o, out_actions ? out_actions + o : nullptr,
+                                          out_margin ? out_margin + o : nullptr)))
+                return rc;
+        }
+        return EBRL_OK;
+    }
     // batch-size class: rows n .. nc-1 decode the padding env; every tile,
     // split and reduction choice of the kernels depends on the problem shape
     // only, so the real rows' bits do not depend on the padding

@@ -929,7 +929,7 @@ struct GemmPlan {
 
 // Kernel and split choice.  The tile variant never changes an element's
 // summation order; the split count (decode only) is a function of (N, K).
-constexpr int SPLIT_MAX_M = 256;
+constexpr int SPLIT_MAX_M = DECODE_MAX_ROWS;
 
 // Macro tile of the large-M kernel: 256 x 256 (16 waves), 192 x 256 (12
 // waves) or 128 x 128 (4 waves, two workgroups per CU).  Each is priced as

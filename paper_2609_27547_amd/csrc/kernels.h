@@ -48,6 +48,9 @@ struct GemmArgs {
     // EPI_RESID: also store the updated rows in bf16 here (nullable).
     void* xb = nullptr; int ldxb = 0;
 };
+// Decode GEMMs (split_ok) plan their K splits for at most this many rows;
+// callers that need batch-size-independent bits keep calls within it.
+constexpr int DECODE_MAX_ROWS = 256;
 // Returns the number of K splits used (1 = single pass).
 int gemm(const GemmArgs& a, hipStream_t s);
 int gemm_splits(bool bf16, int M, int N, int K, size_t ws_floats, bool split_ok);

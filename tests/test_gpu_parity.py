@@ -606,6 +606,30 @@ TINY_LANG = M.Config("tinylang", bf16=True, n_cams=0, img=32, patch=16, layers=2
                      kv_heads=2, head_dim=64, mlp=256, vocab=100, n_lang=130)
 
 
+def test_decode_calls_above_the_decode_gemm_row_limit_keep_bits():
+    """A decode call of more envs than the decode GEMMs plan for (300 > 256)
+    runs as consecutive calls of at most 256: every env's tokens and margins
+    equal those of the env decoded in a small call, bit for bit, and one env
+    matches the oracle."""
+    o = dataclasses.replace(TINY_LANG, n_lang=12)
+    ids = list(range(300))
+    _, lang = _obs(o, ids, 1011)
+    pol = E.Policy(_ebrl_config(o, 300), seed=0)
+    pol.prefill(ids, images=None, lang_ids=_dev(lang))
+    tok, _, mar = pol.decode_actions(ids)
+    torch.cuda.synchronize()
+    sub = [299, 5, 150, 257]
+    tok_s, _, mar_s = pol.decode_actions(sub)
+    torch.cuda.synchronize()
+    for j, e in enumerate(sub):
+        assert torch.equal(tok_s[j], tok[e]) and torch.equal(mar_s[j], mar[e]), e
+    ref = M.Policy(o, seed=0)
+    st = ref.prefill(None, lang[257])
+    r = ref.decode(st, forced=tok[257, :-1].cpu().numpy())
+    P.check_tokens(tok[257].cpu().numpy(), r)
+    pol.close()
+
+
 @pytest.mark.parametrize("hd", [64, 128])
 def test_bf16_attention_at_block_and_tile_boundaries(hd):
     """Language-only bf16 prefixes on either side of the 16-token cache
