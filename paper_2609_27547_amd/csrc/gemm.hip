@@ -9,7 +9,7 @@
 //  * gemm_bf16_big_kernel (M >= 256: prefill, ViT, flow expert): 256 x 256
 //    tiles, 16 waves, operands DMA'd global -> LDS, epilogue staged through
 //    LDS for whole-row stores.
-//  * gemm_bf16_decode_kernel (decode, M <= 256): 64-column slices, per-wave
+//  * gemm_bf16_decode_kernel (decode, M <= 256): 32-, 64- or 96-column slices, per-wave
 //    LDS pipelines fed by whole-line DMA; K split across workgroups only for
 //    narrow outputs, the partials summed in split order inside the kernel by
 //    the last workgroup of each tile.
@@ -497,7 +497,7 @@ __global__ __launch_bounds__(64 * WM * WN, WM * WN == 4 ? 2 : 1) void gemm_bf16_
 
 // ------------------------------------------- bf16 GEMM, decode-sized M --
 // M <= 256 (one row per environment), K % 64 == 0.  A workgroup owns a
-// 64-column slice of the output, at most 64 rows (further row tiles in more
+// 32-, 64- or 96-column slice of the output, at most 64 rows (further row tiles in more
 // workgroups) and a contiguous range of 64-wide K groups; the range is the
 // whole K unless the column slices alone are too few to occupy the chip.  The
 // four waves split that range and run independent pipelines: each wave
@@ -512,7 +512,7 @@ __global__ __launch_bounds__(64 * WM * WN, WM * WN == 4 ? 2 : 1) void gemm_bf16_
 // workgroup that finishes a tile last (a device-scope counter per tile) sums
 // the partials in split order, runs the epilogue and clears the counter for
 // the next call.  An element's summation order depends only on (N, K).
-constexpr int DEC_BN = 64;   // column slice of the split rule (the kernel also runs 32-wide slices)
+constexpr int DEC_BN = 64;   // column slice of the split rule (the kernel also runs 32- and 96-wide slices)
 constexpr int DEC_MAX_SPLITS = 16;
 constexpr int DEC_TILE_FLOATS = 64 * 64;   // partial-tile stride in the workspace
 constexpr int DEC_MAX_COUNTERS = 4096;
@@ -566,6 +566,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_decode_kernel(
     __shared__ int s_last;
     __shared__ float s_ssq[NORM ? 4 : 1][NORM ? TM * 16 : 1];
     static_assert(4 * FR * 64 * 16 <= (int)(sizeof(sW0) + sizeof(sX0)), "reduction buffer");
+    static_assert(FR * 64 * 4 <= DEC_TILE_FLOATS, "partial tile");
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -999,6 +1000,22 @@ static GemmPlan plan_gemm(bool bf16, int M, int N, int K, size_t ws_floats, bool
         p.m_tiles = (M + 16 * p.tm - 1) / (16 * p.tm);
         // 32-column slices when that still leaves under 3/4 of the chip idle
         p.dbn = (long)tiles_n * p.splits * p.m_tiles < 192 ? 32 : 64;
+        // 96-column slices (fragment pairs stay whole; two LDS buffers) for
+        // one row tile of at most 32 rows, when they take fewer rounds of
+        // one workgroup per CU: priced as rounds x the bytes a workgroup
+        // streams per K element (weight plus activation rows).  A CU's DMA
+        // stream runs at about the same rate for either width, so the last,
+        // partly filled round is what the wider slice saves: 7B-class gate/up
+        // (22016 outputs: 344 slices of 64 = 1.34 rounds, 230 of 96 = one)
+        // measured 20-24 % faster at 1-32 rows; narrower outputs (one round
+        // either way) lose.  The slice width never changes a sum's order.
+        if (p.dbn == 64 && p.tm <= 2 && p.m_tiles == 1) {
+            auto cost = [&](int bn) {
+                const long wgs = (long)((N + bn - 1) / bn) * p.splits;
+                return ((wgs + 255) / 256) * (bn + 16 * p.tm);
+            };
+            if (cost(96) < cost(64)) p.dbn = 96;
+        }
         return p;
     }
     if (bf16 && !split_ok && M >= 256 && K % 64 == 0) {
@@ -1053,11 +1070,14 @@ static void launch_bf16(const GemmArgs& a, const GemmPlan& p, Epi epi, hipStream
                                a.counters, a.norm_eps, epi);
         };
         // Non-temporal weight loads where each weight slice is read by a
-        // single workgroup (one row tile) of 64-column slices: measured 5-13 %
+        // single workgroup (one row tile) of 64- or 96-column slices: measured 5-13 %
         // faster there, slower where row tiles or narrow slices re-read it.
         auto pick = [&](auto NORM) {
             constexpr bool NM = decltype(NORM)::value;
-            if (p.dbn == 32) {
+            if (p.dbn == 96) {   // one row tile (plan_gemm)
+                if (p.tm == 1) godec(gemm_bf16_decode_kernel<1, 96, true, NM, PAIRED, Epi>, 96);
+                else godec(gemm_bf16_decode_kernel<2, 96, true, NM, PAIRED, Epi>, 96);
+            } else if (p.dbn == 32) {
                 if (p.tm == 1) godec(gemm_bf16_decode_kernel<1, 32, false, NM, PAIRED, Epi>, 32);
                 else if (p.tm == 2) godec(gemm_bf16_decode_kernel<2, 32, false, NM, PAIRED, Epi>, 32);
                 else godec(gemm_bf16_decode_kernel<4, 32, false, NM, PAIRED, Epi>, 32);

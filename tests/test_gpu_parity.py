@@ -79,13 +79,15 @@ def test_gemm_matches_oracle_linear(M_, N, K, dtype):
     assert P.row_rel_err(C.cpu().numpy(), ref) < 2e-6
 
 
-@pytest.mark.parametrize("N,K", [(3072, 1024), (1024, 4096), (4096, 11008), (8192, 1024), (12288, 4096)])
+@pytest.mark.parametrize("N,K", [(3072, 1024), (1024, 4096), (4096, 11008), (8192, 1024), (12288, 4096),
+                                 (22016, 4096)])
 def test_decode_gemm_repeat_and_row_subsets_bitwise(N, K):
     """Decode-sized GEMMs split K across workgroups; the per-tile completion
     counters must be back at zero after each call (a repeated call gives the
     same bits), and a row's result must not depend on how many rows the call
     holds (batch invariance) -- also where wide outputs switch from 64-row to
-    128-row tiles above 64 rows."""
+    128-row tiles above 64 rows, and where the 22016-wide output runs
+    96-column slices up to 32 rows and 64-column slices above."""
     rng = np.random.default_rng(N + K)
     A = torch.from_numpy(rng.normal(size=(200, K)).astype(np.float32)).to(torch.bfloat16).cuda()
     B = torch.from_numpy(rng.normal(size=(N, K)).astype(np.float32)).to(torch.bfloat16).cuda()
