@@ -563,20 +563,34 @@ __global__ __launch_bounds__(256) void gemm_bf16_decode_kernel(
     __shared__ __attribute__((aligned(1024))) bf16_t sX1[4 * XE];
     __shared__ __attribute__((aligned(1024))) bf16_t sW2[STAGES == 3 ? 4 * WE : 1];
     __shared__ __attribute__((aligned(1024))) bf16_t sX2[STAGES == 3 ? 4 * XE : 1];
-    __shared__ int s_last;
-    __shared__ float s_ssq[NORM ? 4 : 1][NORM ? TM * 16 : 1];
-    static_assert(4 * FR * 64 * 16 <= (int)(sizeof(sW0) + sizeof(sX0)), "reduction buffer");
-    static_assert(FR * 64 * 4 <= DEC_TILE_FLOATS, "partial tile");
+    // After the main loop (every DMA landed, a barrier passed) the staging
+    // buffers hold the waves' tiles for the reduction -- wave w's region in
+    // sW0, then sX0, then sW1, none straddling two buffers -- and sX1 holds
+    // the per-row sums of squares and the last-workgroup flag (96-column
+    // slices of 64 rows fill the whole 160 KB with the two stages).
+    constexpr int RB = FR * 64 * 16;   // bytes of one wave's tile
+    constexpr int CW = (int)sizeof(sW0) / RB, CX = (int)sizeof(sX0) / RB;
+    static_assert(CW + CX + CW >= 4, "reduction buffer");
+    static_assert((NORM ? 4 * TM * 16 * 4 : 0) + 4 <= (int)sizeof(sX1), "row sums and flag");
+    float (*const s_ssq)[TM * 16] = reinterpret_cast<float (*)[TM * 16]>(sX1);
+    int* const s_last = reinterpret_cast<int*>(sX1) + 4 * TM * 16;
+    // K-split partial tiles are DEC_TILE_FLOATS apart in the workspace: the
+    // plan splits K only for kernels whose tile fits that stride.
+    constexpr bool SPLITTABLE = FR * 64 * 4 <= DEC_TILE_FLOATS;
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int r = lane & 15, g = lane >> 4;
     const int tiles_n = (N + BN - 1) / BN;
-    // XCD-aware order: the row tiles of one (column slice, split) pair --
-    // which read the same weights -- run on the same XCD.
+    // XCD-aware order: the dispatcher deals workgroup ids round-robin over
+    // the 8 XCDs; XCD x takes the x-th contiguous range of units (the first
+    // nb % 8 ranges one longer), so the row tiles of one (column slice,
+    // split) pair -- which read the same weights -- run on the same XCD.
     int bid = blockIdx.x;
-    const int nb = gridDim.x;
-    if ((nb & 7) == 0) bid = (bid & 7) * (nb >> 3) + (bid >> 3);
+    {
+        const int nb = gridDim.x, x = bid & 7;
+        bid = x * (nb >> 3) + min(x, nb & 7) + (bid >> 3);
+    }
     const int mt = bid % m_tiles;
     const int unit = bid / m_tiles;
     const int split = unit % splits, nt = unit / splits;
@@ -687,9 +701,12 @@ __global__ __launch_bounds__(256) void gemm_bf16_decode_kernel(
 
     // waves' tiles through LDS (the staging buffers, once every wave is done)
     __syncthreads();
-    f32x4* red = (wave * FR * 64 * 16 < (int)sizeof(sW0))
-                     ? reinterpret_cast<f32x4*>(sW0) + wave * FR * 64
-                     : reinterpret_cast<f32x4*>(sX0) + (wave * FR * 64 - (int)sizeof(sW0) / 16);
+    auto red_region = [&](int w) -> f32x4* {
+        if (w < CW) return reinterpret_cast<f32x4*>(sW0) + w * FR * 64;
+        if (w < CW + CX) return reinterpret_cast<f32x4*>(sX0) + (w - CW) * FR * 64;
+        return reinterpret_cast<f32x4*>(sW1) + (w - CW - CX) * FR * 64;
+    };
+    f32x4* const red = red_region(wave);
 #pragma unroll
     for (int i = 0; i < TM; ++i)
 #pragma unroll
@@ -705,11 +722,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_decode_kernel(
         }
     }
     __syncthreads();
-    auto red_at = [&](int w, int e) -> f32x4 {
-        const int idx = w * FR * 64 + e;
-        return idx * 16 < (int)sizeof(sW0) ? reinterpret_cast<const f32x4*>(sW0)[idx]
-                                            : reinterpret_cast<const f32x4*>(sX0)[idx - (int)sizeof(sW0) / 16];
-    };
+    auto red_at = [&](int w, int e) -> f32x4 { return red_region(w)[e]; };
 
     // Output units: one fragment lane (or a gate/up fragment pair) each.
     constexpr int G = PAIRED ? 2 : 1;
@@ -729,7 +742,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_decode_kernel(
         }
     }
 
-    if (splits > 1) {
+    if (SPLITTABLE && splits > 1) {
         // A workgroup waits for its own partial stores to complete before it
         // bumps the counter; the last one reads the partials only after
         // seeing the final count.
@@ -749,10 +762,10 @@ __global__ __launch_bounds__(256) void gemm_bf16_decode_kernel(
         asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
         __syncthreads();
         if (tid == 0)
-            s_last = __hip_atomic_fetch_add(counters + tile, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
-                     (unsigned)(splits - 1);
+            *s_last = __hip_atomic_fetch_add(counters + tile, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
+                      (unsigned)(splits - 1);
         __syncthreads();
-        if (!s_last) return;
+        if (!*s_last) return;
         // all splits' loads in flight at once, then summed in split order
 #pragma unroll
         for (int q = 0; q < PER; ++q) {
@@ -1000,18 +1013,20 @@ static GemmPlan plan_gemm(bool bf16, int M, int N, int K, size_t ws_floats, bool
         p.m_tiles = (M + 16 * p.tm - 1) / (16 * p.tm);
         // 32-column slices when that still leaves under 3/4 of the chip idle
         p.dbn = (long)tiles_n * p.splits * p.m_tiles < 192 ? 32 : 64;
-        // 96-column slices (fragment pairs stay whole; two LDS buffers) for
-        // one row tile of at most 32 rows, when they take fewer rounds of
-        // one workgroup per CU: priced as rounds x the bytes a workgroup
-        // streams per K element (weight plus activation rows).  A CU's DMA
-        // stream runs at about the same rate for either width, so the last,
-        // partly filled round is what the wider slice saves: 7B-class gate/up
-        // (22016 outputs: 344 slices of 64 = 1.34 rounds, 230 of 96 = one)
-        // measured 20-24 % faster at 1-32 rows; narrower outputs (one round
-        // either way) lose.  The slice width never changes a sum's order.
-        if (p.dbn == 64 && p.tm <= 2 && p.m_tiles == 1) {
+        // 96-column slices (fragment pairs stay whole; two LDS buffers) when
+        // they take fewer rounds of one workgroup per CU: priced as rounds x
+        // the bytes a workgroup streams per K element (weight plus
+        // activation rows).  A CU's DMA stream runs at about the same rate
+        // for either width, so the last, partly filled round is what the
+        // wider slice saves: 7B-class gate/up (22016 outputs: 344 slices of
+        // 64 = 1.34 rounds, 230 of 96 = one) measured 20-24 % faster at 1-32
+        // rows; narrower outputs (one round either way) lose.  Row tiles of
+        // 64 with 96 columns fill the LDS and leave no partial-tile stride
+        // for K splits; smaller row tiles take 96 columns with one row tile
+        // only.  The slice width never changes a sum's order.
+        if (p.dbn == 64 && (p.tm == 4 ? p.splits == 1 : p.m_tiles == 1)) {
             auto cost = [&](int bn) {
-                const long wgs = (long)((N + bn - 1) / bn) * p.splits;
+                const long wgs = (long)((N + bn - 1) / bn) * p.splits * p.m_tiles;
                 return ((wgs + 255) / 256) * (bn + 16 * p.tm);
             };
             if (cost(96) < cost(64)) p.dbn = 96;
@@ -1074,9 +1089,11 @@ static void launch_bf16(const GemmArgs& a, const GemmPlan& p, Epi epi, hipStream
         // faster there, slower where row tiles or narrow slices re-read it.
         auto pick = [&](auto NORM) {
             constexpr bool NM = decltype(NORM)::value;
-            if (p.dbn == 96) {   // one row tile (plan_gemm)
+            if (p.dbn == 96) {   // row tiles of 16 or 32 rows: one tile (plan_gemm)
                 if (p.tm == 1) godec(gemm_bf16_decode_kernel<1, 96, true, NM, PAIRED, Epi>, 96);
-                else godec(gemm_bf16_decode_kernel<2, 96, true, NM, PAIRED, Epi>, 96);
+                else if (p.tm == 2) godec(gemm_bf16_decode_kernel<2, 96, true, NM, PAIRED, Epi>, 96);
+                else if (p.m_tiles == 1) godec(gemm_bf16_decode_kernel<4, 96, true, NM, PAIRED, Epi>, 96);
+                else godec(gemm_bf16_decode_kernel<4, 96, false, NM, PAIRED, Epi>, 96);
             } else if (p.dbn == 32) {
                 if (p.tm == 1) godec(gemm_bf16_decode_kernel<1, 32, false, NM, PAIRED, Epi>, 32);
                 else if (p.tm == 2) godec(gemm_bf16_decode_kernel<2, 32, false, NM, PAIRED, Epi>, 32);

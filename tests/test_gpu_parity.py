@@ -86,8 +86,8 @@ def test_decode_gemm_repeat_and_row_subsets_bitwise(N, K):
     counters must be back at zero after each call (a repeated call gives the
     same bits), and a row's result must not depend on how many rows the call
     holds (batch invariance) -- also where wide outputs switch from 64-row to
-    128-row tiles above 64 rows, and where the 22016-wide output runs
-    96-column slices up to 32 rows and 64-column slices above."""
+    128-row tiles above 64 rows, and where outputs switch between 64- and
+    96-column slices (12288 wide: 64 columns up to 64 rows, 96 above)."""
     rng = np.random.default_rng(N + K)
     A = torch.from_numpy(rng.normal(size=(200, K)).astype(np.float32)).to(torch.bfloat16).cuda()
     B = torch.from_numpy(rng.normal(size=(N, K)).astype(np.float32)).to(torch.bfloat16).cuda()
