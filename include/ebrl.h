@@ -127,7 +127,10 @@ int ebrl_stream_destroy(void* stream);
 
 /* Paper: Section 4.3.1 (the generation stage runs inside its quota).
  * All later calls on p enqueue on `stream` (a hipStream_t on p's device;
- * NULL = the null stream). */
+ * NULL = the null stream).  For a stream made by
+ * ebrl_stream_create_cu_masked (and not yet destroyed) the GEMMs size their
+ * tiles for the CUs its mask selects; results are bitwise the same on any
+ * stream. */
 int ebrl_policy_bind_stream(ebrl_policy* p, void* stream);
 
 /* Paper: Section 2.1 (the backbone fuses observations into the KV cache the

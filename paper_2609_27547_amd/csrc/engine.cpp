@@ -29,6 +29,11 @@ namespace {
 
 thread_local std::string g_create_error;
 
+// CU count of every stream made by ebrl_stream_create_cu_masked (the bits set
+// in its mask), read by the policies bound to it for the GEMM plan.
+std::mutex g_stream_mu;
+std::map<hipStream_t, int> g_stream_cus;
+
 struct LayerW {
     void* qkv = nullptr;   // [(hq + 2 hkv) hd, d]: q rows, then k rows, then v rows
     void* o = nullptr;     // [d, hq hd]
@@ -52,6 +57,8 @@ struct ebrl_policy {
     uint64_t seed = 0;
     int device = 0;
     hipStream_t stream = nullptr;
+    int dev_cus = 256;   // compute units of the device
+    int cus = 256;       // ... that the bound stream may use
     std::string err;
     bool failed = false;
 
@@ -141,7 +148,8 @@ struct ebrl_policy {
     hipEvent_t cur_a = nullptr;
 
     // HIP graphs of whole decode / denoise calls, keyed by the call's batch
-    // size class (decode) or batch size (denoise) only: the per-call metadata
+    // size class (decode) or batch size (denoise) and the bound stream's CU
+    // count (which picks GEMM tile shapes) only: the per-call metadata
     // lives at fixed offsets of meta_dev and is refreshed by an async copy
     // before each launch, and inputs and outputs pass through policy-owned
     // buffers outside the graph, so new caller pointers never re-capture
@@ -464,6 +472,7 @@ int run_gemm(ebrl_policy* p, GemmArgs a, bool split_ok = false) {
     a.ws = p->ws;
     a.ws_floats = p->ws_floats;
     a.counters = p->counters;
+    a.cus = p->cus;
     const int cls = a.M >= 256 ? EBRL_K_GEMM : EBRL_K_GEMM_SKINNY;
     prof_begin(p, cls);
     ebrl::gemm(a, p->stream);
@@ -712,7 +721,8 @@ int denoise(ebrl_policy* p, const int32_t* env_ids, int32_t n, const float* fnoi
     // graph per (batch size, which noises are drawn on the device); the key
     // holds no caller pointer and no prefix length (the attention reads each
     // sequence's length from the metadata)
-    const std::vector<uint64_t> key = {2, (uint64_t)n, (uint64_t)(anoise ? 1 : 0), (uint64_t)(fnoise ? 1 : 0)};
+    const std::vector<uint64_t> key = {2, (uint64_t)n, (uint64_t)(anoise ? 1 : 0), (uint64_t)(fnoise ? 1 : 0),
+                                       (uint64_t)p->cus};
     const int inside = (1 << EBRL_K_GEMM) | (1 << EBRL_K_GEMM_SKINNY) | (1 << EBRL_K_ATTN_PREFILL) |
                        (1 << EBRL_K_OTHER);
     if ((rc = run_graph(p, key, inside, body))) return rc;
@@ -809,6 +819,9 @@ int ebrl_policy_create(const ebrl_config* config, uint64_t seed, ebrl_policy** o
         delete p;
         return fail(nullptr, EBRL_E_HIP, "no HIP device");
     }
+    int ncu = 0;
+    if (hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, p->device) == hipSuccess && ncu > 0)
+        p->dev_cus = p->cus = ncu;
     auto bail = [&](int rc) {
         g_create_error = p->err;
         ebrl_policy_destroy(p);
@@ -1048,12 +1061,22 @@ int ebrl_stream_create_cu_masked(int32_t device, const uint32_t* cu_mask, uint32
         g_create_error = std::string("hipExtStreamCreateWithCUMask: ") + hipGetErrorString(e);
         return EBRL_E_HIP;
     }
+    int bits = 0;
+    for (uint32_t w = 0; w < n_words; ++w) bits += __builtin_popcount(cu_mask[w]);
+    {
+        std::lock_guard<std::mutex> lk(g_stream_mu);
+        g_stream_cus[s] = bits;
+    }
     *out_stream = (void*)s;
     return EBRL_OK;
 }
 
 int ebrl_stream_destroy(void* stream) {
     if (!stream) return EBRL_E_INVALID;
+    {
+        std::lock_guard<std::mutex> lk(g_stream_mu);
+        g_stream_cus.erase((hipStream_t)stream);
+    }
     return hipStreamDestroy((hipStream_t)stream) == hipSuccess ? EBRL_OK : EBRL_E_HIP;
 }
 
@@ -1062,6 +1085,14 @@ int ebrl_policy_bind_stream(ebrl_policy* p, void* stream) {
     if (rc) return rc;
     HIPCHK(p, hipStreamSynchronize(p->stream));
     p->stream = (hipStream_t)stream;
+    // GEMM tile choices (never their sums' order) follow the CUs the stream
+    // may use; decode and denoise graphs are cached per CU count
+    p->cus = p->dev_cus;
+    {
+        std::lock_guard<std::mutex> lk(g_stream_mu);
+        auto it = g_stream_cus.find(p->stream);
+        if (it != g_stream_cus.end() && it->second > 0) p->cus = std::min(it->second, p->dev_cus);
+    }
     return EBRL_OK;
 }
 
@@ -1305,7 +1336,7 @@ int ebrl_decode_actions(ebrl_policy* p, const int32_t* env_ids, int32_t n, int32
         }
         return check_launch(p);
     };
-    const std::vector<uint64_t> key = {1, (uint64_t)nc};
+    const std::vector<uint64_t> key = {1, (uint64_t)nc, (uint64_t)p->cus};
     const int inside = (1 << EBRL_K_GEMM_SKINNY) | (1 << EBRL_K_ATTN_DECODE) | (1 << EBRL_K_OTHER) |
                        (nc >= 256 ? (1 << EBRL_K_GEMM) : 0);
     if ((rc = run_graph(p, key, inside, body))) return rc;

@@ -17,9 +17,12 @@
 //    (K not a multiple of 64), with split-K partials reduced in split order
 //    by splitk_reduce_kernel.
 // fp32 path (fp32 policies): LDS-tiled FMA kernel with the same epilogues.
-// Every tile and split choice is a function of (N, K) -- plus M >= 256 for
-// the large-M kernel -- so results do not depend on timing, on the number of
-// compute units or on how many rows a decode call holds.
+// Every choice that orders a sum -- the K split count -- is a function of
+// (N, K) alone (plus M >= 256 for the large-M kernel); tile shapes, slice
+// widths and block order, which may follow M and the stream's CU count,
+// never change an element's summation order.  Results therefore do not
+// depend on timing, on the number of compute units or on how many rows a
+// decode call holds.
 #include <type_traits>
 
 #include "kernels.h"
@@ -935,7 +938,8 @@ __global__ void splitk_reduce_kernel(const float* __restrict__ ws, int splits, i
 
 // ------------------------------------------------------------- dispatch --
 
-// Tile and split choice depend only on (M, N, K).
+// Tile and split choice depend only on (M, N, K) and the stream's CU count;
+// the split count, the only one that orders sums, on (N, K) alone.
 struct GemmPlan {
     int bm; int bn; int splits; int k_per_split; bool big;
     bool dec; int steps_per_split; int tm; int m_tiles; int dbn;   // decode kernel (steps: 64-wide K groups)
@@ -947,14 +951,14 @@ constexpr int SPLIT_MAX_M = DECODE_MAX_ROWS;
 
 // Macro tile of the large-M kernel: 256 x 256 (16 waves), 192 x 256 (12
 // waves) or 128 x 128 (4 waves, two workgroups per CU).  Each is priced as
-// the number of rounds its tiles take over the 256 CUs times one round's
+// the number of rounds its tiles take over the stream's CUs times one round's
 // work per CU, divided by the variant's throughput relative to 256 x 256
 // (measured: 0.85 and 0.8); the cheapest wins, ties to the larger tile.  The
 // smaller tiles pay off where 256 x 256 tiles leave most of a last round
 // idle (e.g. 576 tiles = 2.25 rounds).  Every variant runs the same K loop,
 // so an element's summation order does not depend on the choice.
-static void big_tile(int M, int N, int& bm, int& bn) {
-    constexpr int CUS = 256;
+static void big_tile(int M, int N, int cus, int& bm, int& bn) {
+    const int CUS = cus;
     struct V { int bm, bn, per_cu; double rel; } vs[] = {{256, 256, 1, 1.0}, {192, 256, 1, 0.85}, {128, 128, 2, 0.8}};
     double best = 0;
     for (int i = 0; i < 3; ++i) {
@@ -970,7 +974,7 @@ static void big_tile(int M, int N, int& bm, int& bn) {
     }
 }
 
-static GemmPlan plan_gemm(bool bf16, int M, int N, int K, size_t ws_floats, bool split_ok) {
+static GemmPlan plan_gemm(bool bf16, int M, int N, int K, size_t ws_floats, bool split_ok, int cus = 256) {
     GemmPlan p;
     p.big = false;
     p.dec = false;
@@ -1011,8 +1015,8 @@ static GemmPlan plan_gemm(bool bf16, int M, int N, int K, size_t ws_floats, bool
         if ((long)tiles_n * p.splits >= 128) p.tm = M <= 16 ? 1 : (M <= 32 ? 2 : 4);
         else p.tm = M <= 64 ? 1 : (M <= 128 ? 2 : 4);
         p.m_tiles = (M + 16 * p.tm - 1) / (16 * p.tm);
-        // 32-column slices when that still leaves under 3/4 of the chip idle
-        p.dbn = (long)tiles_n * p.splits * p.m_tiles < 192 ? 32 : 64;
+        // 32-column slices when that still leaves under 3/4 of the CUs idle
+        p.dbn = (long)tiles_n * p.splits * p.m_tiles < 3L * cus / 4 ? 32 : 64;
         // 96-column slices (fragment pairs stay whole; two LDS buffers) when
         // they take fewer rounds of one workgroup per CU: priced as rounds x
         // the bytes a workgroup streams per K element (weight plus
@@ -1027,7 +1031,7 @@ static GemmPlan plan_gemm(bool bf16, int M, int N, int K, size_t ws_floats, bool
         if (p.dbn == 64 && (p.tm == 4 ? p.splits == 1 : p.m_tiles == 1)) {
             auto cost = [&](int bn) {
                 const long wgs = (long)((N + bn - 1) / bn) * p.splits * p.m_tiles;
-                return ((wgs + 255) / 256) * (bn + 16 * p.tm);
+                return ((wgs + cus - 1) / cus) * (bn + 16 * p.tm);
             };
             if (cost(96) < cost(64)) p.dbn = 96;
         }
@@ -1035,7 +1039,7 @@ static GemmPlan plan_gemm(bool bf16, int M, int N, int K, size_t ws_floats, bool
     }
     if (bf16 && !split_ok && M >= 256 && K % 64 == 0) {
         p.big = true;
-        big_tile(M, N, p.bm, p.bn);
+        big_tile(M, N, cus, p.bm, p.bn);
         return p;
     }
     if (!bf16) p.bm = 64;
@@ -1170,7 +1174,8 @@ static void launch_f32(const GemmArgs& a, const GemmPlan& p, Epi epi, hipStream_
 template <bool PAIRED, class Epi>
 static int dispatch(const GemmArgs& a, Epi epi, hipStream_t s) {
     const GemmPlan p = plan_gemm(a.bf16, a.M, a.N, a.K, a.ws_floats,
-                                 a.split_ok && a.M <= SPLIT_MAX_M && (!a.bf16 || a.counters));
+                                 a.split_ok && a.M <= SPLIT_MAX_M && (!a.bf16 || a.counters),
+                                 std::max(1, std::min(a.cus, 256)));
     if (a.bf16) launch_bf16<PAIRED>(a, p, epi, s);
     else launch_f32<PAIRED>(a, p, epi, s);
     return p.splits;

@@ -47,6 +47,11 @@ struct GemmArgs {
     bool row_norm = false; float norm_eps = 1e-6f;
     // EPI_RESID: also store the updated rows in bf16 here (nullable).
     void* xb = nullptr; int ldxb = 0;
+    // Compute units the launch stream may use (its CU mask): the decode
+    // kernel's column-slice width and the large-M kernel's macro tile are
+    // priced in rounds over this many CUs.  Neither choice changes an
+    // element's summation order.
+    int cus = 256;
 };
 // Decode GEMMs (split_ok) plan their K splits for at most this many rows;
 // callers that need batch-size-independent bits keep calls within it.
