@@ -405,6 +405,55 @@ def test_small_bf16_decode_bitwise_beside_gemm_load(small):
         E.destroy_stream(s_load)
 
 
+def _quarter_mask(q):
+    """CU mask of q quarters of the 256 CUs: 8-CU runs, q of every 4, so the
+    share holds the same part of every XCD."""
+    a = [0] * 8
+    for i in range(256):
+        if (i // 8) % 4 < q:
+            a[i // 32] |= 1 << (i % 32)
+    return a
+
+
+def test_small_bf16_prefill_and_decode_on_cu_shares_bitwise(small):
+    """GEMM tile shapes follow the bound stream's CU count (the large-M
+    kernel's macro tile, the decode kernel's column slices) while the order
+    of every sum does not: prefill and decode on a quarter and on three
+    quarters of the CUs reproduce the whole chip's cache rows, hidden states,
+    tokens, actions and margins bit for bit."""
+    cfg, ids, img, lang, pol, tok, ref, _ = small
+    img_d, lang_d = _dev(img), _dev(lang)
+    tok_f, act_f, mar_f = pol.decode_actions(ids)
+    torch.cuda.synchronize()
+    probe = [0, 31, 63]
+
+    def snap():
+        return [(pol.read_state(E.STATE_H_LAST_PRE, e), pol.read_state(E.STATE_K, e, cfg.layers - 1),
+                 pol.read_state(E.STATE_V, e, 0)) for e in probe]
+
+    base = snap()
+    try:
+        for q in (1, 3):
+            s = E.create_cu_masked_stream(0, _quarter_mask(q))
+            try:
+                pol.bind_stream(s)
+                pol.prefill(ids, images=img_d, lang_ids=lang_d)
+                t2, a2, m2 = pol.decode_actions(ids)
+                torch.cuda.ExternalStream(s).synchronize()
+                assert torch.equal(t2, tok_f) and torch.equal(a2, act_f) and torch.equal(m2, mar_f), q
+                for (h0, k0, v0), (h1, k1, v1) in zip(base, snap()):
+                    assert np.array_equal(h0, h1) and np.array_equal(k0, k1) and np.array_equal(v0, v1), q
+            finally:
+                pol.bind_stream(torch.cuda.current_stream().cuda_stream)
+                torch.cuda.synchronize()
+                E.destroy_stream(s)
+    finally:
+        # the module's other tests read this policy's caches: leave them as
+        # the whole-chip prefill wrote them
+        pol.prefill(ids, images=img_d, lang_ids=lang_d)
+        torch.cuda.synchronize()
+
+
 # ------------------------------------------------------------ tiny flow --
 
 TINY_FLOW = M.Config("tinyflow", bf16=True, n_cams=1, img=32, patch=16, layers=2, d=128, q_heads=4,
