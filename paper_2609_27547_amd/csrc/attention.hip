@@ -3,8 +3,9 @@
 // h / (q_heads / kv_heads).
 //
 // attn_prefill_bf16: flash attention for prefill, the ViT and the flow
-//   expert.  A workgroup (4 waves) owns 64 query rows of one head; 64-key K
-//   and V tiles are DMA'd from the paged cache into double-buffered LDS
+//   expert.  A workgroup (4 waves) owns 64 query rows of one head; K and V
+//   tiles (32 keys at hd 128, 64 at hd 64) are DMA'd from the paged cache
+//   into double-buffered LDS
 //   (whole 128/256-byte rows, XOR-swizzled 16-byte chunks).  Each wave
 //   computes S^T = K Q^T for its 16 queries with v_mfma_f32_16x16x32_bf16 so
 //   that every lane holds the scores of a single query, runs the online
@@ -61,22 +62,23 @@ EBRL_DEV float attn_sum_xor16_32(float v) {
     return __builtin_bit_cast(float, (unsigned)b[0]) + __builtin_bit_cast(float, (unsigned)b[1]);
 }
 
-// One 64-key tile of the online-softmax attention for the wave's 16
-// queries (lane (r, g): query r, keys 16 kt + 4 g + v): scores S^T = K Q^T on
-// MFMA, masking, the integer running maximum, P, and O^T += V^T P^T.  tk / tv
-// point at the tile's K and V rows in LDS (64 rows of HD, 16-byte chunks
-// swizzled by row).
-template <int HD>
+// One KT-key tile (a multiple of 32) of the online-softmax attention for the
+// wave's 16 queries (lane (r, g): query r, keys 16 kt + 4 g + v): scores
+// S^T = K Q^T on MFMA, masking, the integer running maximum, P, and
+// O^T += V^T P^T.  tk / tv point at the tile's K and V rows in LDS (KT rows
+// of HD, 16-byte chunks swizzled by row).
+template <int HD, int KT>
 EBRL_DEV void attn_tile_math(const bf16_t* tk, const bf16_t* tv, int k0, int mask_from, int key_lim,
                              float scale_log2, const bf16x8 (&qb)[HD / 32], float& m_i, float& l_i,
                              f32x4 (&acc)[HD / 16], int lane)
 {
-    constexpr int KT = 64, CPR = HD / 8;
+    static_assert(KT % 32 == 0, "whole 32-key MFMA steps");
+    constexpr int NKT = KT / 16, CPR = HD / 8;
     const int r = lane & 15, g = lane >> 4;
     // S^T tiles: lane holds key 16kt + 4g + v for query r
-    f32x4 s[4];
+    f32x4 s[NKT];
 #pragma unroll
-    for (int kt = 0; kt < 4; ++kt) {
+    for (int kt = 0; kt < NKT; ++kt) {
         s[kt] = f32x4{0.f, 0.f, 0.f, 0.f};
         const int row = kt * 16 + r;
 #pragma unroll
@@ -95,13 +97,13 @@ EBRL_DEV void attn_tile_math(const bf16_t* tk, const bf16_t* tv, int k0, int mas
         // 16 kt + v < lim
         const int lim = key_lim - k0 - 4 * g;
 #pragma unroll
-        for (int kt = 0; kt < 4; ++kt)
+        for (int kt = 0; kt < NKT; ++kt)
 #pragma unroll
             for (int v = 0; v < 4; ++v) s[kt][v] = kt * 16 + v < lim ? s[kt][v] : -INFINITY;
     }
     float tmax = -INFINITY;
 #pragma unroll
-    for (int kt = 0; kt < 4; ++kt)
+    for (int kt = 0; kt < NKT; ++kt)
 #pragma unroll
         for (int v = 0; v < 4; ++v) tmax = fmaxf(tmax, s[kt][v]);
     tmax = attn_max_xor16_32(tmax);
@@ -114,7 +116,7 @@ EBRL_DEV void attn_tile_math(const bf16_t* tk, const bf16_t* tv, int k0, int mas
     const float alpha = (m_i == -INFINITY) ? 0.f : ldexpf(1.0f, (int)(m_i - m_use));
     float psum = 0.f;
 #pragma unroll
-    for (int kt = 0; kt < 4; ++kt)
+    for (int kt = 0; kt < NKT; ++kt)
 #pragma unroll
         for (int v = 0; v < 4; ++v) {
             const float p = fast_exp2(fmaf(s[kt][v], scale_log2, -m_use));
@@ -137,7 +139,7 @@ EBRL_DEV void attn_tile_math(const bf16_t* tk, const bf16_t* tv, int k0, int mas
     // order the score lanes hold.
     const int a16 = lane & 15;
 #pragma unroll
-    for (int ks2 = 0; ks2 < 2; ++ks2) {
+    for (int ks2 = 0; ks2 < KT / 32; ++ks2) {
         bf16x8 pb;
 #pragma unroll
         for (int v = 0; v < 4; ++v) {
@@ -166,19 +168,27 @@ EBRL_DEV void attn_tile_math(const bf16_t* tk, const bf16_t* tv, int k0, int mas
     }
 }
 
+// s_waitcnt on the vector-memory counter only (gfx9 encoding: expcnt and
+// lgkmcnt fields at their maxima).
+template <int N> EBRL_DEV void attn_wait_vmcnt() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt((N & 15) | 0x70 | 0xF00 | ((N >> 4) << 14));
+}
+
 // One workgroup per (query tile of ATTN_Q_TILE rows, head): NW waves of 16
 // queries share every K/V tile staged in LDS, which each wave then skips if
-// none of its queries can see it.
-template <int HD, int NW>
+// none of its queries can see it.  Key tiles of KT keys in an S-buffer ring:
+// S - 1 tiles are in flight while one is multiplied.
+template <int HD, int NW, int KT, int S>
 __global__ __launch_bounds__(64 * NW) void attn_prefill_bf16_kernel(AttnPrefillArgs a, float scale_log2)
 {
     static_assert(16 * NW == ATTN_Q_TILE, "query tile");
-    constexpr int KT = 64;                 // keys per tile
+    static_assert(S >= 2 && S <= 4, "ring depth");
     constexpr int CPR = HD / 8;            // 16-byte chunks per K/V row
     constexpr int RPI = 64 / CPR;          // rows per DMA instruction
     constexpr int TILE = KT * HD;          // bf16 per K (or V) tile
-    __shared__ __attribute__((aligned(1024))) bf16_t sK[2][TILE];
-    __shared__ __attribute__((aligned(1024))) bf16_t sV[2][TILE];
+    __shared__ __attribute__((aligned(1024))) bf16_t sK[S][TILE];
+    __shared__ __attribute__((aligned(1024))) bf16_t sV[S][TILE];
     __shared__ int s_bt[ATTN_BT_MAX];
 
     // Workgroup order: the dispatcher deals workgroup ids round-robin over
@@ -238,11 +248,13 @@ __global__ __launch_bounds__(64 * NW) void attn_prefill_bf16_kernel(AttnPrefillA
     // c stored at chunk position q * CPR + (c ^ (q % CPR)) -- the XOR spans
     // every chunk of a row, so that 8 (hd 64) or 16 (hd 128) consecutive rows
     // put a given chunk on all 64 LDS banks; the waves split the
-    // tile's 64 / RPI instructions for K and the same for V, so that wave w
-    // fills rows 16 w .. 16 w + 15, i.e. exactly one 16-token cache block.
+    // tile's KT / RPI instructions for K and the same for V, so that wave w
+    // fills rows RW w .. RW w + RW - 1, which lie in one 16-token cache block.
+    constexpr int RW = KT / NW;              // rows per wave
     static_assert((KT / RPI) % NW == 0, "DMA split");
-    static_assert(KT == 16 * NW && KV_BLOCK == 16, "one cache block per wave and tile");
+    static_assert(KV_BLOCK == 16 && 16 % RW == 0 && KT % 16 == 0, "a wave's rows in one cache block");
     constexpr int NI = KT / RPI;             // instructions per operand
+    constexpr int IPT = 2 * (NI / NW);       // DMA instructions per tile and wave (K and V)
     const size_t blk_elems = (size_t)2 * hkv * KV_BLOCK * HD;
     const bf16_t* kbase = (const bf16_t*)a.kv.base + (size_t)kvh * KV_BLOCK * HD;
     const size_t voff = (size_t)hkv * KV_BLOCK * HD;
@@ -250,8 +262,8 @@ __global__ __launch_bounds__(64 * NW) void attn_prefill_bf16_kernel(AttnPrefillA
     const uint32_t sv_addr = (uint32_t)(uintptr_t)(attn_lds_ptr_t)&sV[0][0];
     const int row_in = lane / CPR, cpos = lane % CPR;
     auto dma = [&](int it, int buf) {
-        const int blk_key0 = it * KT + wave * 16;     // first key of this wave's block
-        if (blk_key0 + 16 <= kv_end) {
+        const int blk_key0 = it * KT + wave * RW;     // first key of this wave's rows
+        if (blk_key0 + RW <= kv_end) {
             // whole block in range: its address is uniform over the wave
             const int blk = __builtin_amdgcn_readfirstlane(s_bt[blk_key0 >> 4]);
             const bf16_t* kb = kbase + (size_t)blk * blk_elems;
@@ -260,7 +272,7 @@ __global__ __launch_bounds__(64 * NW) void attn_prefill_bf16_kernel(AttnPrefillA
                 const int ins = wave * (NI / NW) + u;
                 const int q = ins * RPI + row_in;
                 const int c = cpos ^ (q & (CPR - 1));
-                const bf16_t* src = kb + (size_t)((q & 15) * HD + c * 8);
+                const bf16_t* src = kb + (size_t)(((it * KT + q) & 15) * HD + c * 8);
                 const uint32_t off = (uint32_t)(buf * TILE + ins * 512) * 2;
                 attn_dma16(src, __builtin_amdgcn_readfirstlane(sk_addr + off));
                 attn_dma16(src + voff, __builtin_amdgcn_readfirstlane(sv_addr + off));
@@ -291,11 +303,15 @@ __global__ __launch_bounds__(64 * NW) void attn_prefill_bf16_kernel(AttnPrefillA
     // every fragment address is a per-lane base plus an immediate offset).
     auto tile = [&](int it, auto BUF) {
         constexpr int buf = decltype(BUF)::value;
-        // tile `it` has landed for every wave, and every wave is done with
-        // tile it - 1, whose buffer the next DMA refills
-        __builtin_amdgcn_s_waitcnt(0);
+        // this wave's part of tile `it` has landed (the tiles issued after it
+        // may stay in flight); after the barrier every wave's part has, and
+        // every wave is done with tile it - 1, whose buffer the next DMA refills
+        const int later = min(S - 2, ntiles - 1 - it);
+        if (later >= 2) attn_wait_vmcnt<2 * IPT>();
+        else if (later == 1) attn_wait_vmcnt<IPT>();
+        else attn_wait_vmcnt<0>();
         __syncthreads();
-        if (it + 1 < ntiles) dma(it + 1, buf ^ 1);
+        if (it + S - 1 < ntiles) dma(it + S - 1, (buf + S - 1) % S);
         const bf16_t* tk = sK[buf];
         const bf16_t* tv = sV[buf];
         const int k0 = it * KT;
@@ -303,13 +319,19 @@ __global__ __launch_bounds__(64 * NW) void attn_prefill_bf16_kernel(AttnPrefillA
         // (processing it would leave m, l and acc as they are)
         if (k0 >= wave_keys) return;
 
-        attn_tile_math<HD>(tk, tv, k0, mask_from, key_lim, scale_log2, qb, m_i, l_i, acc, lane);
+        attn_tile_math<HD, KT>(tk, tv, k0, mask_from, key_lim, scale_log2, qb, m_i, l_i, acc, lane);
     };
 
-    if (ntiles > 0) dma(0, 0);
-    for (int it = 0; it < ntiles; it += 2) {
+    for (int p = 0; p < S - 1 && p < ntiles; ++p) dma(p, p);
+    for (int it = 0; it < ntiles; it += S) {
         tile(it, std::integral_constant<int, 0>{});
         if (it + 1 < ntiles) tile(it + 1, std::integral_constant<int, 1>{});
+        if constexpr (S > 2) {
+            if (it + 2 < ntiles) tile(it + 2, std::integral_constant<int, 2 % S>{});
+        }
+        if constexpr (S > 3) {
+            if (it + 3 < ntiles) tile(it + 3, std::integral_constant<int, 3 % S>{});
+        }
     }
 
     if (qvalid) {
@@ -385,8 +407,12 @@ void attn_prefill(const AttnPrefillArgs& a, hipStream_t s) {
         const float scale_log2 = 1.4426950408889634f / sqrtf((float)hd);
         dim3 grid(a.n_tiles * a.q_heads);
         constexpr int NW = ATTN_Q_TILE / 16;
-        if (hd == 64) hipLaunchKernelGGL((attn_prefill_bf16_kernel<64, NW>), grid, dim3(64 * NW), 0, s, a, scale_log2);
-        else hipLaunchKernelGGL((attn_prefill_bf16_kernel<128, NW>), grid, dim3(64 * NW), 0, s, a, scale_log2);
+        // hd 128: 32-key tiles (32 KB of LDS: up to four workgroups per CU)
+        // measured 9-15 % faster than 64-key tiles; hd 64 keeps 64-key tiles
+        // (32-key ones 3 % slower).  Deeper rings (three 64-key or four 32-key
+        // buffers) were slower at both widths.
+        if (hd == 64) hipLaunchKernelGGL((attn_prefill_bf16_kernel<64, NW, 64, 2>), grid, dim3(64 * NW), 0, s, a, scale_log2);
+        else hipLaunchKernelGGL((attn_prefill_bf16_kernel<128, NW, 32, 2>), grid, dim3(64 * NW), 0, s, a, scale_log2);
     } else {
         const float scale = 1.0f / sqrtf((float)hd);
         dim3 grid(a.n_tiles, a.q_heads, ATTN_Q_TILE);
