@@ -38,7 +38,7 @@ WORKLOADS = {
     "ragged-7b": (3, 128, 1005),
 }
 # default oracle sample per workload: envs that take roughly 10-40 s on the host
-CPU_SAMPLE = {"tiny-fp32": 8, "small-bf16": 32, "7b-bf16": 1, "flow-bf16": 3, "wam-bf16": 2, "ragged-7b": 2}
+CPU_SAMPLE = {"tiny-fp32": 8, "small-bf16": 32, "7b-bf16": 1, "flow-bf16": 3, "wam-bf16": 2, "ragged-7b": 1}
 PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA
 PEAK_FP32_TFLOPS = 157.3      # MI355X fp32 vector
 PEAK_HBM_GBS = 8000.0
