@@ -97,7 +97,7 @@ def test_decode_gemm_repeat_and_row_subsets_bitwise(N, K):
     E.op_gemm(A, B, again)
     torch.cuda.synchronize()
     assert torch.equal(full, again)
-    for m in [1, 7, 16, 17, 40, 64, 130]:
+    for m in [1, 7, 16, 17, 32, 33, 40, 64, 65, 128, 130]:
         C = torch.empty((m, N), dtype=torch.float32, device="cuda")
         E.op_gemm(A[:m].contiguous(), B, C)
         torch.cuda.synchronize()
