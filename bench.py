@@ -652,11 +652,17 @@ def main():
     traffic = stored_traffic(args.workload) if dominant == E.K_GEMM else None
     roofline.update({"frac": round(achieved / roofline["peak"], 4),
                      "traffic": traffic["traffic_bytes_per_launch"] if traffic else None,
-                     "kernel": {E.K_GEMM: "gemm_bf16_big_kernel (projections, M >= 256)",
-                                E.K_GEMM_SKINNY: "gemm_bf16_decode_kernel (decode projections, split-K reduced in-kernel)",
-                                E.K_ATTN_PREFILL: "attn_prefill_bf16_kernel",
-                                E.K_ATTN_DECODE: "attn_decode_bf16_kernel",
-                                E.K_OTHER: "row-wise kernels"}[dominant],
+                     "kernel": ({E.K_GEMM: "gemm_bf16_big_kernel (projections, M >= 256)",
+                                 E.K_GEMM_SKINNY: "gemm_bf16_decode_kernel (decode projections, split-K reduced in-kernel)",
+                                 E.K_ATTN_PREFILL: "attn_prefill_bf16_kernel",
+                                 E.K_ATTN_DECODE: "attn_decode_bf16_kernel",
+                                 E.K_OTHER: "row-wise kernels"} if bf16 else
+                                {E.K_GEMM: "gemm_f32_kernel (projections)",
+                                 E.K_GEMM_SKINNY: "gemm_f32_kernel (decode projections, split-K partials summed by "
+                                                  "splitk_reduce_kernel)",
+                                 E.K_ATTN_PREFILL: "attn_prefill_f32_kernel",
+                                 E.K_ATTN_DECODE: "attn_decode_split_kernel + attn_decode_combine_kernel",
+                                 E.K_OTHER: "row-wise kernels"})[dominant],
                      "launches": dom["launches"],
                      "avg_launch_us": round(1000 * dom["ms"] / max(1, dom["launches"]), 2),
                      "share_of_step": round(dom["ms"] / (gpu_ms_instr if graphed else gpu_ms), 3) if gpu_ms else None,
