@@ -60,6 +60,18 @@ def stored_traffic(workload: str):
     return t if t.get("sources_sha") == pmc_traffic.sources_hash() else None
 
 
+def cpu_model() -> str:
+    """The host CPU's model name (Linux /proc/cpuinfo), or "unknown"."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(workload: str, n_sample: int):
     """The oracle as it stands, on this host's cores, on n_sample envs of the
     same workload (envs are independent, so the rate scales per env)."""
@@ -94,7 +106,7 @@ def cpu_baseline(workload: str, n_sample: int):
         for st in states:
             pol.decode(st)
         dt = time.perf_counter() - t
-        return {"value": round(len(ids) / dt, 4), "unit": "actions/s", "cores": int(cores), "kind": "oracle",
+        return {"value": round(len(ids) / dt, 4), "unit": "actions/s", "cores": int(cores), "cpu": cpu_model(), "kind": "oracle",
                 "sample": f"{len(ids)} env(s) of the first ragged call (prefixes of "
                           f"{', '.join(str(int(T[e])) for e in ids)} tokens): 6 decode steps each in float64 "
                           f"(numpy/BLAS), {dt:.1f} s; weight generation ({t_w:.1f} s) and the pool's prefill excluded",
@@ -112,7 +124,7 @@ def cpu_baseline(workload: str, n_sample: int):
             pol.decode(st)
     dt = time.perf_counter() - t
     what = "prefill + 10 Euler steps of the expert" if cfg.exp_layers else "prefill + 6 decode steps"
-    return {"value": round(n_sample * per_env / dt, 4), "unit": "actions/s", "cores": int(cores), "kind": "oracle",
+    return {"value": round(n_sample * per_env / dt, 4), "unit": "actions/s", "cores": int(cores), "cpu": cpu_model(), "kind": "oracle",
             "sample": f"{n_sample} env(s) of the same workload: {what} in float64 (numpy/BLAS), {dt:.1f} s; "
                       f"weight generation ({t_w:.1f} s) excluded",
             "seconds": round(dt, 3)}
