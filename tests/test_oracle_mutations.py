@@ -1,0 +1,267 @@
+"""Planted mistakes in the CPU oracle (no GPU).
+
+Each mutant replaces one oracle function or method with a plausible slip --
+a dropped term, a wrong sign, index, axis or position, a transposed or
+swapped operand -- and the pins of test_oracle_pins.py must fail on it.
+This checks the pins rather than the oracle: a mutant that every pin lets
+through would mark a gap in them.  The mutants live here, in test code; the
+oracle itself is never edited.
+"""
+
+
+import numpy as np
+import pytest
+
+from tests import test_oracle_pins as PINS
+from oracle import model as M
+
+# ------------------------------------------------------- building blocks --
+
+
+def _rope(sign=1.0, adjacent=False, theta_scale=2.0):
+    def rope(x, pos, base=10000.0):
+        hd = x.shape[-1]
+        half = hd // 2
+        i = np.arange(half, dtype=np.float64)
+        theta = base ** (-theta_scale * i / hd)
+        ang = pos.astype(np.float64)[:, None] * theta[None, :]
+        c = np.cos(ang)[:, None, :]
+        s = sign * np.sin(ang)[:, None, :]
+        if adjacent:
+            x1, x2 = x[..., 0::2], x[..., 1::2]
+            out = np.empty_like(x)
+            out[..., 0::2] = x1 * c - x2 * s
+            out[..., 1::2] = x2 * c + x1 * s
+            return out
+        x1, x2 = x[..., :half], x[..., half:]
+        return np.concatenate([x1 * c - x2 * s, x2 * c + x1 * s], axis=-1)
+    return rope
+
+
+def _attention(scale="sqrt", strict=False, swap_kv=False):
+    def attention(q, k, v, q_pos, k_pos, causal):
+        hd = q.shape[-1]
+        s = q @ k.T
+        if scale == "sqrt":
+            s = s / np.sqrt(hd)
+        elif scale == "hd":
+            s = s / hd
+        if causal:
+            mask = (k_pos[None, :] < q_pos[:, None]) if strict else (k_pos[None, :] <= q_pos[:, None])
+            s = np.where(mask, s, -np.inf)
+        return M.softmax(s) @ (k if swap_kv else v)
+    return attention
+
+
+def _mha_modulo(q, k, v, q_pos, k_pos, causal):
+    hq, hkv = q.shape[1], k.shape[1]
+    out = np.empty_like(q)
+    for h in range(hq):
+        g = h % hkv
+        out[:, h, :] = M.attention(q[:, h, :], k[:, g, :], v[:, g, :], q_pos, k_pos, causal)
+    return out
+
+
+def _patchify(col_major=False, inner_transposed=False):
+    def patchify(image, p):
+        cams, h, w, c = image.shape
+        out = []
+        for cam in range(cams):
+            cells = [(py, px) for px in range(w // p) for py in range(h // p)] if col_major else \
+                    [(py, px) for py in range(h // p) for px in range(w // p)]
+            for py, px in cells:
+                t = image[cam, py * p:(py + 1) * p, px * p:(px + 1) * p, :]
+                if inner_transposed:
+                    t = t.transpose(1, 0, 2)
+                out.append(t.reshape(-1))
+        return np.asarray(out, dtype=np.float64)
+    return patchify
+
+
+def _argmax_highest(logits):
+    best = 0
+    for i in range(1, len(logits)):
+        if logits[i] >= logits[best]:
+            best = i
+    return best
+
+
+def _time_embedding(swap=False, freq_dim=False):
+    def time_embedding(tau, dim):
+        half = dim // 2
+        j = np.arange(half, dtype=np.float64)
+        w = 10000.0 ** (-j / (dim if freq_dim else half))
+        a = 1000.0 * tau * w
+        return np.concatenate([np.cos(a), np.sin(a)] if swap else [np.sin(a), np.cos(a)])
+    return time_embedding
+
+
+def _euler(sign=-1.0, reversed_tau=False):
+    def euler_integrate(x0, velocity, n_steps):
+        x = x0
+        for k in range(n_steps):
+            tau = k / n_steps if reversed_tau else 1.0 - k / n_steps
+            x = x + sign * velocity(x, tau) / n_steps
+        return x
+    return euler_integrate
+
+
+# ------------------------------------------------------------ the block --
+
+
+def _block(slip):
+    """Policy.block with one slip; every other line as in the oracle,
+    including its bf16 storage points."""
+    def block(self, x, Wl, n_heads, n_kv, hd, pos, past_k=None, past_v=None, past_pos=None,
+              causal=True, use_rope=True):
+        t = x.shape[0]
+        R = self._r
+        h = self._prenorm(x)
+        q = M.linear(h, Wl["q"]).reshape(t, n_heads, hd)
+        k = M.linear(h, Wl["k"]).reshape(t, n_kv, hd)
+        v = M.linear(h, Wl["k" if slip == "v_from_k" else "v"]).reshape(t, n_kv, hd)
+        if use_rope:
+            q = M.rope(q, pos, self.cfg.rope_base)
+            if slip != "rope_q_only":
+                k = M.rope(k, pos, self.cfg.rope_base)
+        q, k, v = R(q, "q"), R(k, "kv"), R(v, "kv")
+        if past_k is not None:
+            K = np.concatenate([past_k, k], axis=0)
+            V = np.concatenate([past_v, v], axis=0)
+            kpos = np.concatenate([past_pos, pos])
+        else:
+            K, V, kpos = k, v, pos
+        if "p" in self.bf16_points:
+            o = self._attention_bf16(q, K, V, pos, kpos, causal)
+        else:
+            o = M.multihead_attention(q, K, V, pos, kpos, causal)
+        o = R(o.reshape(t, n_heads * hd), "attn_out")
+        ao = M.linear(o, Wl["o"])
+        x1 = ao if slip == "no_attn_residual" else x + ao
+        h2 = h if slip == "stale_mlp_norm" else self._prenorm(x1)
+        g, u = M.linear(h2, Wl["gate"]), M.linear(h2, Wl["up"])
+        act = M.silu(u) * g if slip == "swiglu_swapped" else M.silu(g) * u
+        x2 = x1 + M.linear(R(act, "swiglu_out"), Wl["down"])
+        return x2, k, v
+    return block
+
+
+# ----------------------------------------------------- decode and experts --
+
+
+def _decode(slip):
+    def decode(self, st, forced=None):
+        cfg = self.cfg
+        n_tok = cfg.n_action_tokens
+        logits = [self.logits(st.h_last)]
+        tokens = [M.argmax_lowest(logits[0])]
+        ks, vs = list(st.k), list(st.v)
+        kpos = np.arange(st.T)
+        E = self.W("E_lang" if slip == "lang_embedding" else "E_act")
+        for step in range(1, n_tok):
+            t_in = tokens[-1] if forced is None else int(forced[step - 1])
+            x = E[t_in][None, :]
+            pos = np.array([st.T + step - (0 if slip == "position_plus_one" else 1)])
+            for l in range(cfg.layers):
+                x, k, v = self.block(x, self.layer("dec", l), cfg.q_heads, cfg.kv_heads,
+                                     cfg.head_dim, pos, ks[l], vs[l], kpos)
+                ks[l] = np.concatenate([ks[l], k], axis=0)
+                vs[l] = np.concatenate([vs[l], v], axis=0)
+            kpos = np.concatenate([kpos, pos])
+            lg = self.logits(x[0] if slip == "unnormed_head" else M.rmsnorm(x[0], cfg.eps))
+            logits.append(lg)
+            tokens.append(M.argmax_lowest(lg))
+        L = np.stack(logits)
+        toks = np.asarray(tokens, dtype=np.int64)
+        return M.DecodeResult(toks, L, np.array([M.top2_margin(r) for r in L]),
+                              M.detokenize(toks, cfg.n_bins))
+    return decode
+
+
+def _velocity(slip):
+    def velocity(self, st, x, tau):
+        cfg = self.cfg
+        h = M.linear(x, self.W("W_ain"))
+        if slip != "no_time_vector":
+            h = h + self.time_vector(tau)[None, :]
+        pos = (0 if slip == "positions_from_zero" else st.T) + np.arange(cfg.chunk)
+        ppos = np.arange(st.T)
+        for l in range(cfg.exp_layers):
+            lk = 0 if slip == "first_layer_cache" else l
+            h, _, _ = self.block(h, self.layer("exp", l), cfg.exp_heads, cfg.exp_heads, cfg.head_dim, pos,
+                                 st.k[lk], st.v[lk], ppos, causal=(slip == "causal_actions"))
+        return M.linear(M.rmsnorm(h, cfg.eps), self.W("W_aout"))
+    return velocity
+
+
+MUTANTS = {
+    # function mutants: (module attribute, replacement)
+    "linear without the transpose": ("linear", lambda x, w: x @ w),
+    "rmsnorm over mean |x|": ("rmsnorm", lambda x, eps=1e-6: x / np.sqrt(np.mean(np.abs(x), axis=-1, keepdims=True) + eps)),
+    "rmsnorm without eps": ("rmsnorm", lambda x, eps=1e-6: x / np.sqrt(np.mean(x * x, axis=-1, keepdims=True))),
+    "rmsnorm over the sum": ("rmsnorm", lambda x, eps=1e-6: x / np.sqrt(np.sum(x * x, axis=-1, keepdims=True) + eps)),
+    "silu with the sign flipped": ("silu", lambda x: x / (1.0 + np.exp(x))),
+    "softmax over the wrong axis": ("softmax", lambda s: np.exp(s - s.max(0, keepdims=True)) /
+                                    np.exp(s - s.max(0, keepdims=True)).sum(0, keepdims=True)),
+    "rope rotating the other way": ("rope", _rope(sign=-1.0)),
+    "rope pairing adjacent dims": ("rope", _rope(adjacent=True)),
+    "rope with theta_i = base^(-i/hd)": ("rope", _rope(theta_scale=1.0)),
+    "attention scaled by 1/hd": ("attention", _attention(scale="hd")),
+    "attention unscaled": ("attention", _attention(scale="none")),
+    "attention mask excluding the diagonal": ("attention", _attention(strict=True)),
+    "attention weighting K instead of V": ("attention", _attention(swap_kv=True)),
+    "grouped heads h % hkv": ("multihead_attention", _mha_modulo),
+    "patches in column-major order": ("patchify", _patchify(col_major=True)),
+    "patch pixels transposed": ("patchify", _patchify(inner_transposed=True)),
+    "argmax ties to the highest index": ("argmax_lowest", _argmax_highest),
+    "top-2 margin against the minimum": ("top2_margin", lambda l: float(np.max(l) - np.min(l))),
+    "detokenize without the half bin": ("detokenize", lambda b, n_bins=256: -1.0 + 2.0 * np.asarray(b, dtype=np.float64) / n_bins),
+    "time embedding cos before sin": ("time_embedding", _time_embedding(swap=True)),
+    "time embedding frequencies over dim": ("time_embedding", _time_embedding(freq_dim=True)),
+    "Euler step with the wrong sign": ("euler_integrate", _euler(sign=1.0)),
+    "Euler time running forward": ("euler_integrate", _euler(reversed_tau=True)),
+    # method mutants: (Policy attribute, replacement)
+    "block: V projected with W_k": ("Policy.block", _block("v_from_k")),
+    "block: rotary on queries only": ("Policy.block", _block("rope_q_only")),
+    "block: attention residual dropped": ("Policy.block", _block("no_attn_residual")),
+    "block: MLP reads the pre-attention norm": ("Policy.block", _block("stale_mlp_norm")),
+    "block: SwiGLU gate and up swapped": ("Policy.block", _block("swiglu_swapped")),
+    "decode: language embedding for action tokens": ("Policy.decode", _decode("lang_embedding")),
+    "decode: positions one too far": ("Policy.decode", _decode("position_plus_one")),
+    "decode: logits of the unnormalised state": ("Policy.decode", _decode("unnormed_head")),
+    "expert: no time vector": ("Policy.velocity", _velocity("no_time_vector")),
+    "expert: action positions from 0": ("Policy.velocity", _velocity("positions_from_zero")),
+    "expert: first layer's prefix cache everywhere": ("Policy.velocity", _velocity("first_layer_cache")),
+    "expert: causal among action tokens": ("Policy.velocity", _velocity("causal_actions")),
+}
+
+
+def _pins():
+    return [(n, f) for n, f in sorted(vars(PINS).items()) if n.startswith("test_") and callable(f)]
+
+
+def _run_pins():
+    caught = []
+    for name, fn in _pins():
+        try:
+            with np.errstate(all="ignore"):
+                fn()
+        except Exception:          # an assertion, or the mutant breaking a shape or a value
+            caught.append(name)
+    return caught
+
+
+def test_pins_pass_on_the_oracle_as_written():
+    assert _run_pins() == []
+
+
+@pytest.mark.parametrize("mutant", sorted(MUTANTS))
+def test_pins_catch_planted_mistake(mutant, monkeypatch):
+    target, repl = MUTANTS[mutant]
+    if target.startswith("Policy."):
+        monkeypatch.setattr(M.Policy, target.split(".", 1)[1], repl)
+    else:
+        monkeypatch.setattr(M, target, repl)
+    caught = _run_pins()
+    print(f"{mutant}: caught by {caught}", flush=True)
+    assert caught, f"no pin fails when the oracle has: {mutant}"

@@ -304,6 +304,31 @@ def test_single_token_block_closed_forms():
     g = h @ Wl["gate"].T
     u = h @ Wl["up"].T
     assert np.allclose(out, x + (g / (1 + np.exp(-g)) * u) @ Wl["down"].T, atol=1e-13)
+    # both branches: the MLP reads the norm of the stream after the
+    # attention residual, x1 = x + rmsnorm(x) Wv^T Wo^T
+    out, _, _ = pol.block(x, Wl, cfg.q_heads, cfg.kv_heads, cfg.head_dim, pos)
+    x1 = x + h @ Wl["v"].T @ Wl["o"].T
+    h1 = M.rmsnorm(x1)
+    g1 = h1 @ Wl["gate"].T
+    u1 = h1 @ Wl["up"].T
+    assert np.allclose(out, x1 + (g1 / (1 + np.exp(-g1)) * u1) @ Wl["down"].T, atol=1e-13)
+
+
+def test_block_output_invariant_to_a_common_position_shift():
+    # rotary scores depend on positions only through their differences and
+    # the causal mask only on their order, so shifting every position of a
+    # sequence by the same amount leaves a block's output unchanged (as long
+    # as queries and keys are rotated alike)
+    cfg = tiny_cfg()
+    pol = M.Policy(cfg, seed=0)
+    Wl = pol.layer("dec", 0)
+    x = np.random.default_rng(8).normal(size=(5, cfg.d))
+    outs = [pol.block(x, Wl, cfg.q_heads, cfg.kv_heads, cfg.head_dim, np.arange(5) + p)[0]
+            for p in (0, 7, 100)]
+    assert np.allclose(outs[1], outs[0], atol=1e-12) and np.allclose(outs[2], outs[0], atol=1e-12)
+    # while the positions do matter: a different spacing changes the output
+    spread = pol.block(x, Wl, cfg.q_heads, cfg.kv_heads, cfg.head_dim, 3 * np.arange(5))[0]
+    assert not np.allclose(spread, outs[0], atol=1e-9)
 
 
 def test_prefix_order_embeddings_and_action_head_closed_form():
