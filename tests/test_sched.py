@@ -29,6 +29,19 @@ def test_oracle_algorithm2_priority():
     assert [S.dispatch() for _ in range(4)] == [1, 2, 0, 3]
 
 
+def test_oracle_algorithm2_ranks_by_the_last_recorded_step():
+    # env 0 steps 5 then 1, env 1 steps 2: by the last recorded durations
+    # (1 vs 2) env 1 goes next; by accumulated time (6 vs 2) env 0 would
+    S = O.Scheduler(2, 1, 3)
+    S.next_group()
+    S.deliver(0)
+    assert [S.dispatch(), S.dispatch()] == [0, 1]
+    assert not S.complete(0, 5.0) and not S.complete(1, 2.0)
+    assert S.dispatch() == 0                             # 5 > 2
+    assert not S.complete(0, 1.0)
+    assert S.dispatch() == 1                             # last steps: 2 > 1
+
+
 def test_oracle_ready_set_and_group_queue():
     S = O.Scheduler(4, 2, 1)
     assert S.next_group() == (0, [0, 1]) and S.next_group() == (1, [2, 3])
