@@ -190,8 +190,56 @@ def _velocity(slip):
             lk = 0 if slip == "first_layer_cache" else l
             h, _, _ = self.block(h, self.layer("exp", l), cfg.exp_heads, cfg.exp_heads, cfg.head_dim, pos,
                                  st.k[lk], st.v[lk], ppos, causal=(slip == "causal_actions"))
-        return M.linear(M.rmsnorm(h, cfg.eps), self.W("W_aout"))
+        return M.linear(h if slip == "no_final_norm" else M.rmsnorm(h, cfg.eps), self.W("W_aout"))
     return velocity
+
+
+def _embed_prefix(slip):
+    def embed_prefix(self, image, lang):
+        cfg = self.cfg
+        rows = []
+        if image is not None:
+            patches = self._r(M.patchify(np.asarray(image, dtype=np.float64), cfg.patch), "gemm_in")
+            if cfg.vit_layers:
+                v = M.linear(patches, self.W("W_pe"))
+                if slip != "vit_without_position":
+                    v = v + self.W("vit_pos")
+                hd = cfg.vit_d // cfg.vit_heads
+                pos = np.arange(v.shape[0])
+                for l in range(cfg.vit_layers):
+                    v, _, _ = self.block(v, self.layer("vit", l), cfg.vit_heads, cfg.vit_heads, hd,
+                                         pos, causal=False, use_rope=False)
+                vn = v if slip == "vit_without_final_norm" else M.rmsnorm(v, cfg.eps)
+                rows.append(M.linear(self._r(vn, "gemm_in"), self.W("W_proj")))
+            else:
+                rows.append(M.linear(patches, self.W("W_pe")))
+        E = self.W("E_lang")
+        if len(lang):
+            lang_rows = E[np.asarray(lang, dtype=np.int64)]
+            if slip == "language_first":
+                rows.insert(0, lang_rows)
+            else:
+                rows.append(lang_rows)
+        return np.concatenate(rows, axis=0)
+    return embed_prefix
+
+
+def _prefill_unnormed(self, image, lang):
+    cfg = self.cfg
+    x = self.embed_prefix(image, lang)
+    T = x.shape[0]
+    pos = np.arange(T)
+    ks, vs = [], []
+    for l in range(cfg.layers):
+        x, k, v = self.block(x, self.layer("dec", l), cfg.q_heads, cfg.kv_heads, cfg.head_dim, pos)
+        ks.append(k)
+        vs.append(v)
+    return M.PrefixState(T, ks, vs, x[-1].copy(), x[-1].copy())
+
+
+def _time_vector_without_silu(self, tau):
+    te = M.time_embedding(tau, self.cfg.exp_d)
+    return M.linear(M.linear(te[None, :], self.W("W_t1")), self.W("W_t2"))[0]
 
 
 MUTANTS = {
@@ -233,6 +281,13 @@ MUTANTS = {
     "expert: action positions from 0": ("Policy.velocity", _velocity("positions_from_zero")),
     "expert: first layer's prefix cache everywhere": ("Policy.velocity", _velocity("first_layer_cache")),
     "expert: causal among action tokens": ("Policy.velocity", _velocity("causal_actions")),
+    "expert: no final norm": ("Policy.velocity", _velocity("no_final_norm")),
+    "expert: time MLP without SiLU": ("Policy.time_vector", _time_vector_without_silu),
+    "prefix: language before the image": ("Policy.embed_prefix", _embed_prefix("language_first")),
+    "prefix: ViT without the position embedding": ("Policy.embed_prefix", _embed_prefix("vit_without_position")),
+    "prefix: ViT without its final norm": ("Policy.embed_prefix", _embed_prefix("vit_without_final_norm")),
+    "prefix: last state left unnormalised": ("Policy.prefill", _prefill_unnormed),
+    "head: action logits from the action embedding": ("Policy.logits", lambda self, h: M.linear(h[None, :], self.W("E_act"))[0]),
 }
 
 
