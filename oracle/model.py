@@ -30,7 +30,10 @@ numpy's matmul, exp, sqrt, sin, cos.  No blocking, fusion or reordering.
 Parity pins for every function live in ``tests/test_oracle_pins.py``.
 The architectural readings themselves (which layers exist, in which order)
 have nothing in the paper to compare against: parity unpinned for the
-architecture choice; only its internal consistency is pinned.
+architecture choice; only its internal consistency is pinned.  One such
+reading no invariant can tell from its alternative: the world action
+model's token order (frame tokens before the action chunk, hence their
+rotary positions) -- parity unpinned.
 """
 from __future__ import annotations
 

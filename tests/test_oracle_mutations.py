@@ -242,6 +242,42 @@ def _time_vector_without_silu(self, tau):
     return M.linear(M.linear(te[None, :], self.W("W_t1")), self.W("W_t2"))[0]
 
 
+def _joint_velocity(slip):
+    def joint_velocity(self, st, xf, xa, tau):
+        cfg = self.cfg
+        F = xf.shape[0]
+        t = self.time_vector(tau)[None, :]
+        hf = M.linear(xf, self.W("W_fin")) + t
+        ha = M.linear(xa, self.W("W_ain")) + t
+        h = np.concatenate([ha, hf] if slip == "actions_first" else [hf, ha], axis=0)
+        pos = st.T + np.arange(F + cfg.chunk)
+        ppos = np.arange(st.T)
+        for l in range(cfg.exp_layers):
+            h, _, _ = self.block(h, self.layer("exp", l), cfg.exp_heads, cfg.exp_heads,
+                                 cfg.head_dim, pos, st.k[l], st.v[l], ppos, causal=False)
+        y = M.rmsnorm(h, cfg.eps)
+        if slip == "actions_first":
+            ya, yf = y[:cfg.chunk], y[cfg.chunk:]
+        else:
+            yf, ya = y[:F], y[F:]
+        return M.linear(yf, self.W("W_fout")), M.linear(ya, self.W("W_aout"))
+    return joint_velocity
+
+
+def _joint_velocity_no_frame_time(self, st, xf, xa, tau):
+    cfg = self.cfg
+    F = xf.shape[0]
+    t = self.time_vector(tau)[None, :]
+    h = np.concatenate([M.linear(xf, self.W("W_fin")), M.linear(xa, self.W("W_ain")) + t], axis=0)
+    pos = st.T + np.arange(F + cfg.chunk)
+    ppos = np.arange(st.T)
+    for l in range(cfg.exp_layers):
+        h, _, _ = self.block(h, self.layer("exp", l), cfg.exp_heads, cfg.exp_heads,
+                             cfg.head_dim, pos, st.k[l], st.v[l], ppos, causal=False)
+    y = M.rmsnorm(h, cfg.eps)
+    return M.linear(y[:F], self.W("W_fout")), M.linear(y[F:], self.W("W_aout"))
+
+
 MUTANTS = {
     # function mutants: (module attribute, replacement)
     "linear without the transpose": ("linear", lambda x, w: x @ w),
@@ -288,6 +324,8 @@ MUTANTS = {
     "prefix: ViT without its final norm": ("Policy.embed_prefix", _embed_prefix("vit_without_final_norm")),
     "prefix: last state left unnormalised": ("Policy.prefill", _prefill_unnormed),
     "head: action logits from the action embedding": ("Policy.logits", lambda self, h: M.linear(h[None, :], self.W("E_act"))[0]),
+    "world model: action tokens before the frames": ("Policy.joint_velocity", _joint_velocity("actions_first")),
+    "world model: frame tokens without the time vector": ("Policy.joint_velocity", _joint_velocity_no_frame_time),
 }
 
 
@@ -310,7 +348,17 @@ def test_pins_pass_on_the_oracle_as_written():
     assert _run_pins() == []
 
 
-@pytest.mark.parametrize("mutant", sorted(MUTANTS))
+# Readings no mathematical fact decides, so no pin can catch their
+# mutants; the GPU path is held to the oracle's choice by the parity tests.
+UNPINNED = {
+    "world model: action tokens before the frames":
+        "the order of frame and action tokens (and so their rotary positions) is a reading",
+}
+
+
+@pytest.mark.parametrize("mutant", [
+    pytest.param(m, marks=pytest.mark.xfail(reason=UNPINNED[m], strict=True)) if m in UNPINNED else m
+    for m in sorted(MUTANTS)])
 def test_pins_catch_planted_mistake(mutant, monkeypatch):
     target, repl = MUTANTS[mutant]
     if target.startswith("Policy."):
