@@ -572,6 +572,38 @@ def test_tiny_wam_bf16_parity_and_closed_forms(exp_d):
     pol.close()
 
 
+
+@pytest.mark.parametrize("model", ["flow", "wam"])
+def test_denoise_batch_invariance_bitwise(model):
+    """An env's denoised action chunk (and frames) do not depend on the call:
+    8 envs (400 / 960 expert rows: the large-M GEMM kernel) against one env
+    (50 / 120 rows: the small-M kernel) and a reordered subset, bit for bit,
+    with the same caller noise."""
+    o = TINY_WAM if model == "wam" else TINY_FLOW
+    frames = model == "wam"
+    ids = list(range(8))
+    img, lang = _obs(o, ids, 1013)
+    na = synth_inputs.flow_noise(6, ids, o.chunk, o.adim)
+    nf = synth_inputs.flow_noise(5, ids, o.frame_tokens, o.frame_dim) if frames else None
+
+    def run(pol, sub):
+        if frames:
+            return pol.wam_denoise(sub, _dev(nf[sub]), _dev(na[sub]))
+        return None, pol.flow_denoise(sub, _dev(na[sub]))
+
+    pol = E.Policy(_ebrl_config(o, 8), seed=0)
+    pol.prefill(ids, images=_dev(img), lang_ids=_dev(lang))
+    f_all, a_all = run(pol, ids)
+    torch.cuda.synchronize()
+    for sub in ([5], [6, 1, 3]):
+        f, a = run(pol, sub)
+        torch.cuda.synchronize()
+        for j, e in enumerate(sub):
+            assert torch.equal(a[j], a_all[e]), (sub, e)
+            if frames:
+                assert torch.equal(f[j], f_all[e]), (sub, e)
+    pol.close()
+
 def test_tiny_wam_seeded_noise_closed_form():
     # both noises drawn by the library, frames on stream 4, one count per
     # env advanced once per call; zero output projections return them as is
