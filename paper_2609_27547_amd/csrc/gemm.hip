@@ -6,9 +6,9 @@
 // output columns of one row: a SwiGLU gate/up pair lands in the same lane
 // (weights packed in 32-row groups: 16 gate rows, then the 16 matching up
 // rows), and so does a rotary pair of the fused QKV projection.
-//  * gemm_bf16_big_kernel (M >= 256: prefill, ViT, flow expert): 256 x 256
-//    tiles, 16 waves, operands DMA'd global -> LDS, epilogue staged through
-//    LDS for whole-row stores.
+//  * gemm_bf16_big_kernel (M >= 256: prefill, ViT, flow expert): 256 x 256,
+//    192 x 256 or 128 x 128 tiles (16, 12 or 8 waves), operands DMA'd
+//    global -> LDS, epilogue staged through LDS for whole-row stores.
 //  * gemm_bf16_decode_kernel (decode, M <= 256): 32-, 64- or 96-column slices, per-wave
 //    LDS pipelines fed by whole-line DMA; K split across workgroups only for
 //    narrow outputs, the partials summed in split order inside the kernel by
@@ -355,7 +355,7 @@ EBRL_DEV bf16x8 lds_frag(const bf16_t* tile, int row, int c) {
 }
 
 template <int BM, int BN, int WM, int WN, bool PAIRED, bool SPLIT, class Epi>
-__global__ __launch_bounds__(64 * WM * WN, WM * WN == 4 ? 2 : 1) void gemm_bf16_big_kernel(
+__global__ __launch_bounds__(64 * WM * WN, WM * WN == 8 ? 4 : 1) void gemm_bf16_big_kernel(
     const bf16_t* __restrict__ A, int lda, const bf16_t* __restrict__ B, int ldb, int M, int N, int K,
     int k_per_split, float* __restrict__ ws, Epi epi)
 {
@@ -448,8 +448,8 @@ __global__ __launch_bounds__(64 * WM * WN, WM * WN == 4 ? 2 : 1) void gemm_bf16_
     // 16-32-byte pieces of 16 rows.  Rows are padded to 68 floats so the
     // fragment-layout writes spread over the banks.
     static_assert(!SPLIT, "the large-M kernel never splits K");
-    static_assert(WTN == 64, "staging assumes 64-column wave tiles");
-    constexpr int SROW = 68;
+    static_assert(WTN == 64 || WTN == 32, "staging assumes 64- or 32-column wave tiles");
+    constexpr int SROW = WTN + 4;
     constexpr int PER_A = (BM * 64 * 2) / (16 * SROW * 4), PER_B = (BN * 64 * 2) / (16 * SROW * 4);
     static_assert(2 * (PER_A + PER_B) >= NW, "staging space");
     static_assert(WTM == 64, "one row per lane in the per-row epilogue data");
@@ -469,11 +469,12 @@ __global__ __launch_bounds__(64 * WM * WN, WM * WN == 4 ? 2 : 1) void gemm_bf16_
             *reinterpret_cast<f32x4*>(stage + r * SROW + j * 16 + 4 * g) = acc[i][j];
         const int mrow0 = m0 + wm * WTM + i * 16;
         if constexpr (PAIRED) {
-            // 8 lanes per row: gate columns c (c % 32 < 16) with up partner c + 16
+            // WTN / 8 lanes per row: gate columns c (c % 32 < 16) with up partner c + 16
+            constexpr int LPR = WTN / 8;
 #pragma unroll
-            for (int pass = 0; pass < 2; ++pass) {
-                const int row = pass * 8 + (lane >> 3);
-                const int c = ((lane >> 2) & 1) * 32 + (lane & 3) * 4;
+            for (int pass = 0; pass < LPR / 4; ++pass) {
+                const int row = pass * (64 / LPR) + lane / LPR;
+                const int c = ((lane % LPR) >> 2) * 32 + (lane & 3) * 4;
                 const f32x4 gv4 = *reinterpret_cast<const f32x4*>(stage + row * SROW + c);
                 const f32x4 uv4 = *reinterpret_cast<const f32x4*>(stage + row * SROW + c + 16);
                 const int m = mrow0 + row, n = ncol0 + c;
@@ -485,10 +486,12 @@ __global__ __launch_bounds__(64 * WM * WN, WM * WN == 4 ? 2 : 1) void gemm_bf16_
                 }
             }
         } else {
+            // WTN / 4 lanes per row, four columns each
+            constexpr int LPR = WTN / 4;
 #pragma unroll
-            for (int pass = 0; pass < 4; ++pass) {
-                const int row = pass * 4 + (lane >> 4);
-                const int c = (lane & 15) * 4;
+            for (int pass = 0; pass < LPR / 4; ++pass) {
+                const int row = pass * (64 / LPR) + lane / LPR;
+                const int c = (lane % LPR) * 4;
                 const f32x4 v = *reinterpret_cast<const f32x4*>(stage + row * SROW + c);
                 const int m = mrow0 + row, n = ncol0 + c;
                 if (m < M && n < N) epi(m, n, v[0], v[1], v[2], v[3]);
@@ -950,7 +953,9 @@ struct GemmPlan {
 constexpr int SPLIT_MAX_M = DECODE_MAX_ROWS;
 
 // Macro tile of the large-M kernel: 256 x 256 (16 waves), 192 x 256 (12
-// waves) or 128 x 128 (4 waves, two workgroups per CU).  Each is priced as
+// waves) or 128 x 128 (8 waves of 64 x 32, two workgroups per CU; with four
+// waves of 64 x 64 instead, one workgroup on a CU kept a single wave per
+// SIMD and ran the flow expert's projections up to 13 % slower).  Each is priced as
 // the number of rounds its tiles take over the stream's CUs times one round's
 // work per CU, divided by the variant's throughput relative to 256 x 256
 // (measured: 0.85 and 0.8); the cheapest wins, ties to the larger tile.  The
@@ -1077,7 +1082,7 @@ static void launch_bf16(const GemmArgs& a, const GemmPlan& p, Epi epi, hipStream
             hipLaunchKernelGGL((gemm_bf16_big_kernel<192, 256, 3, 4, PAIRED, false, Epi>), grid, dim3(768), 0, s,
                                (const bf16_t*)a.A, a.lda, (const bf16_t*)a.B, a.ldb, a.M, a.N, a.K, a.K, a.ws, epi);
         else
-            hipLaunchKernelGGL((gemm_bf16_big_kernel<128, 128, 2, 2, PAIRED, false, Epi>), grid, dim3(256), 0, s,
+            hipLaunchKernelGGL((gemm_bf16_big_kernel<128, 128, 2, 4, PAIRED, false, Epi>), grid, dim3(512), 0, s,
                                (const bf16_t*)a.A, a.lda, (const bf16_t*)a.B, a.ldb, a.M, a.N, a.K, a.K, a.ws, epi);
         return;
     }
