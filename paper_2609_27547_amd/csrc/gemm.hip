@@ -290,7 +290,8 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(
 
 // ------------------------------------------------ bf16 MFMA GEMM, large M --
 // 256 x 256 macro tiles, 16 waves in 4 x 4 (64 x 64 per wave, four waves
-// per SIMD so that one wave's LDS waits overlap another's MFMAs).
+// per SIMD so that one wave's LDS waits overlap another's MFMAs); the
+// 192 x 256 and 128 x 128 variants run 12 waves of 64 x 64 and 8 of 64 x 32.
 // Operands go global -> LDS with global_load_lds_dwordx4 (no VGPR staging):
 // a wave instruction writes 64 lanes x 16 bytes contiguously, so the tile is
 // stored as 16-byte chunks, chunk (row, c) of a 64-element row at position

@@ -133,9 +133,10 @@ def test_op_gemm_concurrent_streams_keep_their_own_split_workspace():
 def test_large_gemm_tile_variants_agree_bitwise():
     """The large-M kernel's macro tile follows the shape: with 4092 columns
     (ragged against both 256 and 128), 9200 rows take 192 x 256 tiles (the
-    last row tile ragged), 4096 rows 256 x 256 and 2048 rows 128 x 128.  The
-    rows the three calls share are bitwise equal (every variant runs the same
-    K order), and the full product matches the definition."""
+    last row tile ragged), 4096 rows 256 x 256, 2048 rows 128 x 128 and 1000
+    rows 128 x 128 with a ragged last row tile (256 tiles, one workgroup per
+    CU).  The rows the calls share are bitwise equal (every variant runs the
+    same K order), and the full product matches the definition."""
     rng = np.random.default_rng(9200)
     K = 192
     a = rng.normal(size=(9200, K)).astype(np.float32)
@@ -143,13 +144,14 @@ def test_large_gemm_tile_variants_agree_bitwise():
     A = torch.from_numpy(a).to(torch.bfloat16).cuda()
     B = torch.from_numpy(b).to(torch.bfloat16).cuda()
     outs = {}
-    for m in (9200, 4096, 2048):
+    for m in (9200, 4096, 2048, 1000):
         C = torch.full((m, 4092), np.nan, dtype=torch.float32, device="cuda")
         E.op_gemm(A[:m].contiguous(), B, C)
         outs[m] = C
     torch.cuda.synchronize()
     assert torch.equal(outs[4096], outs[9200][:4096])
     assert torch.equal(outs[2048], outs[9200][:2048])
+    assert torch.equal(outs[1000], outs[9200][:1000])
     a64 = A.float().cpu().numpy().astype(np.float64)
     b64 = B.float().cpu().numpy().astype(np.float64)
     assert P.row_rel_err(outs[9200].cpu().numpy(), M.linear(a64, b64)) < 2e-6
