@@ -58,7 +58,7 @@ def _ebrl_config(o: M.Config, max_envs: int, max_seq: int = 0) -> "E.Config":
 @pytest.mark.parametrize("M_,N,K", [(1, 64, 64), (16, 256, 64), (17, 128, 72), (64, 3072, 1024),
                                     (100, 192, 1024), (300, 1024, 512), (513, 384, 768), (40, 8192, 1024),
                                     (700, 2304, 256), (1100, 4096, 640), (255, 1024, 4096), (8, 4100, 11008),
-                                    (33, 100, 96), (40, 22016, 4096), (100, 12288, 4096)])
+                                    (33, 100, 96), (40, 22016, 4096), (100, 12288, 4096), (260, 36, 128)])
 @pytest.mark.parametrize("dtype", ["bf16", "fp32"])
 def test_gemm_matches_oracle_linear(M_, N, K, dtype):
     rng = np.random.default_rng(M_ * 7 + N + K)
