@@ -355,7 +355,8 @@ EBRL_DEV bf16x8 lds_frag(const bf16_t* tile, int row, int c) {
     return *reinterpret_cast<const bf16x8*>(tile + row * 64 + ((c ^ (row & 7)) << 3));
 }
 
-template <int BM, int BN, int WM, int WN, bool PAIRED, bool SPLIT, class Epi>
+// XO: the K loop overlaps the per-tile barrier with MFMAs (below).
+template <int BM, int BN, int WM, int WN, bool PAIRED, bool XO, class Epi>
 __global__ __launch_bounds__(64 * WM * WN, WM * WN == 8 ? 4 : 1) void gemm_bf16_big_kernel(
     const bf16_t* __restrict__ A, int lda, const bf16_t* __restrict__ B, int ldb, int M, int N, int K,
     int k_per_split, float* __restrict__ ws, Epi epi)
@@ -397,24 +398,59 @@ __global__ __launch_bounds__(64 * WM * WN, WM * WN == 8 ? 4 : 1) void gemm_bf16_
 #pragma unroll
         for (int j = 0; j < TN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-    // All fragment reads of the K tile are issued first, so the second
-    // half's reads overlap the first half's MFMAs.
-    auto compute = [&](const bf16_t* ta, const bf16_t* tb) {
-        bf16x8 wa[2][TN], xb[2][TM];
+    // Each 64-wide K tile is multiplied as two 32-wide halves.  With XO the
+    // barrier that publishes tile t + 1 sits between tile t's halves: before it a
+    // wave reads tile t's second-half fragments and multiplies its first
+    // half; after it, it issues the DMA of tile t + 2 into the stage tile t
+    // has left, multiplies tile t's second half -- operands already in
+    // registers, so the MFMA pipes start right after the barrier -- and
+    // then reads tile t + 1's first-half fragments behind those MFMAs.
+    // Every accumulator still takes its K steps in order, so the bits do
+    // not depend on XO.  The 16-wave tile has no registers for the second
+    // fragment set (it spills); on 12 waves the overlap measured 4-7 %
+    // faster at K 4096-11008 and 3 % slower at K 1024, on 8 waves 2-6 %
+    // faster at every K.
+    static_assert(!XO || WM * WN != 16, "the 16-wave tile runs without the overlap");
+    bf16x8 w0[TN], x0[TM], w1[TN], x1[TM];
+    auto read_half = [&](const bf16_t* ta, const bf16_t* tb, int ks, bf16x8 (&w)[TN], bf16x8 (&x)[TM]) {
 #pragma unroll
-        for (int ks = 0; ks < 2; ++ks) {
+        for (int j = 0; j < TN; ++j) w[j] = lds_frag(tb, wn * WTN + j * 16 + r, ks * 4 + g);
 #pragma unroll
-            for (int j = 0; j < TN; ++j) wa[ks][j] = lds_frag(tb, wn * WTN + j * 16 + r, ks * 4 + g);
+        for (int i = 0; i < TM; ++i) x[i] = lds_frag(ta, wm * WTM + i * 16 + r, ks * 4 + g);
+    };
+    auto mma = [&](const bf16x8 (&w)[TN], const bf16x8 (&x)[TM]) {
 #pragma unroll
-            for (int i = 0; i < TM; ++i) xb[ks][i] = lds_frag(ta, wm * WTM + i * 16 + r, ks * 4 + g);
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int j = 0; j < TN; ++j)
+                acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w[j], x[i], acc[i][j], 0, 0, 0);
+    };
+    // tile t is in stage (ta, tb), tile t + 1 in (na, nb_); tile t + 2 goes
+    // into (ta, tb)
+    auto step = [&](int t, bf16_t* ta, bf16_t* tb, const bf16_t* na, const bf16_t* nb_) {
+        read_half(ta, tb, 1, w1, x1);
+        mma(w0, x0);
+        __builtin_amdgcn_sched_barrier(0);
+        // own fragment reads of this stage done, own DMA of tile t + 1 landed
+        __builtin_amdgcn_s_waitcnt(0);
+        __builtin_amdgcn_s_barrier();
+        __builtin_amdgcn_sched_barrier(0);
+        if (t + 2 < nk) {
+            load_tile_lds<BM, NW>(A, lda, m0, M, k_begin + (t + 2) * 64, ta, wave, lane);
+            load_tile_lds<BN, NW>(B, ldb, n0, N, k_begin + (t + 2) * 64, tb, wave, lane);
         }
-#pragma unroll
-        for (int ks = 0; ks < 2; ++ks)
-#pragma unroll
-            for (int i = 0; i < TM; ++i)
-#pragma unroll
-                for (int j = 0; j < TN; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wa[ks][j], xb[ks][i], acc[i][j], 0, 0, 0);
+        mma(w1, x1);
+        __builtin_amdgcn_sched_barrier(0);
+        if (t + 1 < nk) read_half(na, nb_, 0, w0, x0);
+    };
+
+    // Without the overlap: a whole K tile's fragments are read, multiplied,
+    // then the wave waits at the barrier.
+    auto compute = [&](const bf16_t* ta, const bf16_t* tb) {
+        read_half(ta, tb, 0, w0, x0);
+        read_half(ta, tb, 1, w1, x1);
+        mma(w0, x0);
+        mma(w1, x1);
     };
 
     if (nk > 0) {
@@ -422,22 +458,34 @@ __global__ __launch_bounds__(64 * WM * WN, WM * WN == 8 ? 4 : 1) void gemm_bf16_
         load_tile_lds<BN, NW>(B, ldb, n0, N, k_begin, sB0, wave, lane);
         wait_vm_all();
         __syncthreads();
-        for (int kt = 0; kt < nk; kt += 2) {
-            if (kt + 1 < nk) {
-                load_tile_lds<BM, NW>(A, lda, m0, M, k_begin + (kt + 1) * 64, sA1, wave, lane);
-                load_tile_lds<BN, NW>(B, ldb, n0, N, k_begin + (kt + 1) * 64, sB1, wave, lane);
-            }
-            compute(sA0, sB0);
-            wait_vm_all();
-            __syncthreads();
-            if (kt + 1 < nk) {
-                if (kt + 2 < nk) {
-                    load_tile_lds<BM, NW>(A, lda, m0, M, k_begin + (kt + 2) * 64, sA0, wave, lane);
-                    load_tile_lds<BN, NW>(B, ldb, n0, N, k_begin + (kt + 2) * 64, sB0, wave, lane);
+        if constexpr (!XO) {
+            for (int kt = 0; kt < nk; kt += 2) {
+                if (kt + 1 < nk) {
+                    load_tile_lds<BM, NW>(A, lda, m0, M, k_begin + (kt + 1) * 64, sA1, wave, lane);
+                    load_tile_lds<BN, NW>(B, ldb, n0, N, k_begin + (kt + 1) * 64, sB1, wave, lane);
                 }
-                compute(sA1, sB1);
+                compute(sA0, sB0);
                 wait_vm_all();
                 __syncthreads();
+                if (kt + 1 < nk) {
+                    if (kt + 2 < nk) {
+                        load_tile_lds<BM, NW>(A, lda, m0, M, k_begin + (kt + 2) * 64, sA0, wave, lane);
+                        load_tile_lds<BN, NW>(B, ldb, n0, N, k_begin + (kt + 2) * 64, sB0, wave, lane);
+                    }
+                    compute(sA1, sB1);
+                    wait_vm_all();
+                    __syncthreads();
+                }
+            }
+        } else {
+            if (nk > 1) {
+                load_tile_lds<BM, NW>(A, lda, m0, M, k_begin + 64, sA1, wave, lane);
+                load_tile_lds<BN, NW>(B, ldb, n0, N, k_begin + 64, sB1, wave, lane);
+            }
+            read_half(sA0, sB0, 0, w0, x0);
+            for (int kt = 0; kt < nk; kt += 2) {
+                step(kt, sA0, sB0, sA1, sB1);
+                if (kt + 1 < nk) step(kt + 1, sA1, sB1, sA0, sB0);
             }
         }
     }
@@ -448,7 +496,6 @@ __global__ __launch_bounds__(64 * WM * WN, WM * WN == 8 ? 4 : 1) void gemm_bf16_
     // read) covers 256-byte fp32 / 64-128-byte bf16 row segments instead of
     // 16-32-byte pieces of 16 rows.  Rows are padded to 68 floats so the
     // fragment-layout writes spread over the banks.
-    static_assert(!SPLIT, "the large-M kernel never splits K");
     static_assert(WTN == 64 || WTN == 32, "staging assumes 64- or 32-column wave tiles");
     constexpr int SROW = WTN + 4;
     constexpr int PER_A = (BM * 64 * 2) / (16 * SROW * 4), PER_B = (BN * 64 * 2) / (16 * SROW * 4);
@@ -1079,11 +1126,14 @@ static void launch_bf16(const GemmArgs& a, const GemmPlan& p, Epi epi, hipStream
         if (p.bm == 256)
             hipLaunchKernelGGL((gemm_bf16_big_kernel<256, 256, 4, 4, PAIRED, false, Epi>), grid, dim3(1024), 0, s,
                                (const bf16_t*)a.A, a.lda, (const bf16_t*)a.B, a.ldb, a.M, a.N, a.K, a.K, a.ws, epi);
+        else if (p.bm == 192 && a.K >= 2048)
+            hipLaunchKernelGGL((gemm_bf16_big_kernel<192, 256, 3, 4, PAIRED, true, Epi>), grid, dim3(768), 0, s,
+                               (const bf16_t*)a.A, a.lda, (const bf16_t*)a.B, a.ldb, a.M, a.N, a.K, a.K, a.ws, epi);
         else if (p.bm == 192)
             hipLaunchKernelGGL((gemm_bf16_big_kernel<192, 256, 3, 4, PAIRED, false, Epi>), grid, dim3(768), 0, s,
                                (const bf16_t*)a.A, a.lda, (const bf16_t*)a.B, a.ldb, a.M, a.N, a.K, a.K, a.ws, epi);
         else
-            hipLaunchKernelGGL((gemm_bf16_big_kernel<128, 128, 2, 4, PAIRED, false, Epi>), grid, dim3(512), 0, s,
+            hipLaunchKernelGGL((gemm_bf16_big_kernel<128, 128, 2, 4, PAIRED, true, Epi>), grid, dim3(512), 0, s,
                                (const bf16_t*)a.A, a.lda, (const bf16_t*)a.B, a.ldb, a.M, a.N, a.K, a.K, a.ws, epi);
         return;
     }
