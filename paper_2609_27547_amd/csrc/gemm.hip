@@ -407,9 +407,9 @@ __global__ __launch_bounds__(64 * WM * WN, WM * WN == 8 ? 4 : 1) void gemm_bf16_
     // then reads tile t + 1's first-half fragments behind those MFMAs.
     // Every accumulator still takes its K steps in order, so the bits do
     // not depend on XO.  The 16-wave tile has no registers for the second
-    // fragment set (it spills); on 12 waves the overlap measured 4-7 %
-    // faster at K 4096-11008 and 3 % slower at K 1024, on 8 waves 2-6 %
-    // faster at every K.
+    // fragment set (it spills); on 12 waves the overlap measured up to 7 %
+    // faster from K 2048 on (one shape 2.5 % slower) and 3 % slower at
+    // K 1024, on 8 waves 2-6 % faster at every K.
     static_assert(!XO || WM * WN != 16, "the 16-wave tile runs without the overlap");
     bf16x8 w0[TN], x0[TM], w1[TN], x1[TM];
     auto read_half = [&](const bf16_t* ta, const bf16_t* tb, int ks, bf16x8 (&w)[TN], bf16x8 (&x)[TM]) {
