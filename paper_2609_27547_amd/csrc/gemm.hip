@@ -327,15 +327,35 @@ EBRL_DEV void dma16_to_lds_nt(const void* g, uint32_t lds_addr) {
 }
 
 
+// The same DMA in its scalar-base form: a wave-uniform 64-bit base in SGPRs
+// plus a 32-bit per-lane byte offset, so a wave's row offsets stay fixed
+// across K tiles (only the scalar base advances) and take one VGPR each.
+EBRL_DEV void dma16_to_lds_s(const void* sbase, uint32_t voff, uint32_t lds_addr) {
+    asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
+                 :: "v"(voff), "s"(sbase), "s"(lds_addr) : "memory", "m0");
+}
+
+// ROWS x 64 bf16 of G (rows row0_g.., columns k0..k0+63; rows past
+// rows_valid repeat the last valid row) into lds_tile, 16-byte chunk c of
+// row r at position r * 8 + (c ^ (r & 7)).  The loads go through inline
+// assembly: callers wait on vmcnt and synchronise before reading the tile.
 template <int ROWS, int NW>
 EBRL_DEV void load_tile_lds(const bf16_t* __restrict__ G, int ld, int row0_g, int rows_valid, int k0,
                             bf16_t* lds_tile, int wave, int lane) {
+    // base and LDS addresses are wave-uniform: pinned to SGPRs (readfirstlane
+    // returns int: each half goes through uint32_t, so the low half is
+    // zero-extended)
+    const uint64_t b = (uint64_t)(uintptr_t)(G + (size_t)row0_g * ld + k0);
+    const uint32_t b_hi = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)(b >> 32));
+    const uint32_t b_lo = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)b);
+    const void* const base = (const void*)(uintptr_t)(((uint64_t)b_hi << 32) | (uint64_t)b_lo);
+    const uint32_t lds0 = (uint32_t)(uintptr_t)(lds_ptr_t)lds_tile;
+    const int last = rows_valid - 1 - row0_g;
     auto group = [&](int r0) {   // rows r0 .. r0+7, one instruction
         const int row = r0 + (lane >> 3);
         const int c = (lane & 7) ^ (row & 7);
-        const int gr = min(row0_g + row, rows_valid - 1);
-        const bf16_t* src = G + (size_t)gr * ld + k0 + c * 8;
-        __builtin_amdgcn_global_load_lds((const void*)src, (lds_ptr_t)(lds_tile + r0 * 64), 16, 0, 0);
+        const uint32_t voff = (uint32_t)(min(row, last) * ld + c * 8) * 2u;
+        dma16_to_lds_s(base, voff, __builtin_amdgcn_readfirstlane(lds0 + (uint32_t)r0 * 128u));
     };
     if constexpr (ROWS % (8 * NW) == 0) {
         // each of the NW waves fills ROWS/NW consecutive rows
@@ -388,7 +408,8 @@ __global__ __launch_bounds__(64 * WM * WN, WM * WN == 8 ? 4 : 1) void gemm_bf16_
     const int k_end = min(K, k_begin + k_per_split);
     const int nk = (k_end - k_begin) / 64;
 
-    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wm = wave / WN, wn = wave - (wave / WN) * WN;
     const int r = lane & 15, g = lane >> 4;
 
