@@ -385,8 +385,9 @@ __global__ __launch_bounds__(64 * WM * WN, WM * WN == 8 ? 4 : 1) void gemm_bf16_
     constexpr int WTM = BM / WM, WTN = BN / WN;
     constexpr int TM = WTM / 16, TN = WTN / 16;
     static_assert(!PAIRED || (TN % 2 == 0), "paired epilogue needs tile pairs");
-    // one __shared__ object per stage, so that the compiler can tell the
-    // stage being read from the stage the DMA is filling
+    // one __shared__ object per stage and operand (the DMA that fills them
+    // is inline assembly the compiler does not track: every read of a stage
+    // follows an explicit vmcnt wait and a barrier)
     __shared__ __attribute__((aligned(1024))) bf16_t sA0[BM * 64];
     __shared__ __attribute__((aligned(1024))) bf16_t sA1[BM * 64];
     __shared__ __attribute__((aligned(1024))) bf16_t sB0[BN * 64];
